@@ -1,0 +1,165 @@
+"""Throughput of the ALTR token-reduction path on one MI355X.
+
+A step is one whole reduction (score -> select -> gather, every kernel of the
+path) of one batch: 64 LLaVA-1.5-style images of 576 tokens x 4096 bf16
+channels (plus their pre-/post-MLP states) reduced to 64 tokens each.  Inputs
+are seeded synthetic tensors resident in HBM before the timed region.
+
+Prints one JSON line with images/s, the roofline of the dominant kernel (the
+fused scoring pass, HBM-bound) and the fp64 CPU oracle timed on the host.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "images/s reducing 576x4096 bf16 to 64 tokens; achieved HBM GB/s vs peak"
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "score_kernel_traffic_llava_b64_576x4096_bf16.md")
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--K", type=int, default=64, choices=[64, 128, 192])
+    ap.add_argument("--images", type=int, default=64)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="target wall time of the oracle sample")
+    return ap.parse_args()
+
+
+def score_source_sha() -> str:
+    h = hashlib.sha256()
+    for f in ("tr_score.hip", "tr_internal.h"):
+        with open(os.path.join(ROOT, "paper_2607_13500_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic():
+    """HBM bytes per score launch from the committed PMC summary, if it is current."""
+    try:
+        text = open(TRAFFIC_PROFILE).read()
+    except OSError:
+        return None
+    sha = re.search(r"source_sha256:\s*([0-9a-f]{64})", text)
+    byt = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not sha or not byt or sha.group(1) != score_source_sha():
+        return None
+    return float(byt.group(1))
+
+
+def cpu_baseline(w, seconds: float):
+    import oracle
+    X, P, Q = w.X.cpu(), w.Xpre.cpu(), w.Xpost.cpu()
+    runs = 0
+    t0 = time.perf_counter()
+    while True:
+        oracle.reduce(X, P, Q, w.N, w.K, w.lam, want_out=True, want_scores=False)
+        runs += 1
+        el = time.perf_counter() - t0
+        if el >= seconds or runs >= 50:
+            break
+    return {"value": runs * w.B / el, "unit": "images/s", "cores": 1, "kind": "oracle",
+            "sample": "%d x the full %d-image batch (fp64 C oracle, one thread, %.1f s)"
+                      % (runs, w.B, el)}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the path has no multi-GPU mode "
+              "(images are independent; see the sharding notes). Run with --gpus 1.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import synth
+    import paper_2607_13500_amd as tr
+
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    w = synth.llava(device=dev, B=args.images, N=576, D=4096, K=args.K)
+    torch.cuda.synchronize()
+    r = tr.Reducer(w.D, w.Dc, w.dtype, lam=w.lam, max_images=w.B, max_tokens=sum(w.N), max_N=576)
+    sk = sum(w.K)
+    out = torch.empty(sk, w.D, dtype=w.dtype, device=dev)
+    idx = torch.empty(sk, dtype=torch.int32, device=dev)
+    src = torch.empty(sk, dtype=torch.uint8, device=dev)
+
+    def step():
+        r.reduce(w.X, w.Xpre, w.Xpost, w.N, w.K, out=out, out_idx=idx, out_src=src)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # Timed region: K whole steps; the library records HIP events around each
+    # of its kernels on the same (current) stream for the per-kernel roofline.
+    r.timing(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    stage_ms, calls = r.timing_read()
+    r.timing(False)
+
+    ms_step = 1e3 * elapsed / args.steps
+    images_s = w.B * args.steps / elapsed
+    rows = sum(w.N)
+    e = w.X.element_size()
+    score_bytes = rows * (w.D + 2 * w.Dc) * e + rows * 8          # read X, X', X''; write 2 keys
+    score_ms = stage_ms[0] / max(calls, 1)
+    achieved = score_bytes / (score_ms * 1e-3) / 1e9
+    path_bytes = w.algorithmic_bytes()
+    traffic = measured_traffic()
+
+    line = {
+        "metric": METRIC,
+        "value": round(images_s, 1),
+        "unit": "images/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "llava-1.5 visual tokens, %d images x 576 tokens x 4096 bf16 -> %d kept"
+                               % (w.B, args.K),
+                   "images": w.B, "tokens_per_image": 576, "D": w.D, "Dc": w.Dc, "K": args.K,
+                   "lambda": round(w.lam, 6)},
+        "tokens_per_s": round(rows * args.steps / elapsed, 1),
+        "path_hbm": {"algorithmic_bytes": path_bytes,
+                     "achieved_GBs": round(path_bytes / (ms_step * 1e-3) / 1e9, 1),
+                     "frac": round(path_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
+        "stage_ms": {"score": round(stage_ms[0] / max(calls, 1), 5),
+                     "select": round(stage_ms[1] / max(calls, 1), 5),
+                     "gather": round(stage_ms[2] / max(calls, 1), 5)},
+        "roofline": {"kernel": "score_kernel", "bound": "hbm", "achieved": round(achieved, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": traffic, "algorithmic_bytes_per_launch": score_bytes},
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+    r.close()
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

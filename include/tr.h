@@ -1,0 +1,177 @@
+/*
+ * tr.h - C ABI of the MI355X (gfx950) ALTR visual-token reduction library.
+ *
+ * The operation (the paper's Sec. "Methodology", Eq. (3)-(7), Algorithm 1):
+ * for every image b of a packed batch with N_b tokens x_i (rows of X) and the
+ * pre-/post-MLP states x'_i, x''_i of the vision encoder's last MLP (rows of
+ * X_pre and X_post, Eq. (5)), keep K_b tokens:
+ *   1. K1 = floor(lambda K_b), K2 = K_b - K1                  (Algorithm 1)
+ *   2. H2(x_i) = -log sum_j p_ij^2, p_ij = |x_ij| / sum_k |x_ik|   (Eq. 3-4)
+ *   3. X^imp = the K1 tokens of highest H2 (ties: lower index)
+ *   4. s_i = cos(x'_i, x''_i)                                      (Eq. 6)
+ *   5. sort X^rem = X \ X^imp by s ascending (ties: lower index first)
+ *   6. t = max(1, floor(|X^rem| / K2)); X^div = sorted positions 0, t, ...,
+ *      (K2-1) t                                                (Algorithm 1)
+ *   7. X* = X^imp U X^div (Eq. 7), listed in ascending token index, and the
+ *      kept rows of X gathered into a compact output.
+ *
+ * Readings where the paper is silent: natural log; an all-zero row of X has
+ * H2 = 0; a zero-norm x' or x'' gives s = 0; non-finite inputs give
+ * unspecified (but memory-safe) results.
+ *
+ * Arithmetic: scores are accumulated in fp32 from exactly widened inputs.
+ * Stage I ranks by the squared coefficient of variation of |x| (CV^2), which
+ * orders tokens exactly as H2 does (H2 = log D - log(1 + CV^2)) and keeps
+ * near-uniform rows apart in fp32.  Selection and gather are exact integer
+ * and byte work.  A token row's scores depend only on its own bytes, so
+ * identical rows tie exactly and resolve by index.
+ *
+ * Memory: every pointer named "device" is HIP device memory on the device
+ * that was current at tr_create; host arrays are read during the call only.
+ * The caller owns all tensors; a context owns only the scratch it allocates
+ * in tr_create.  tr_reduce and tr_select allocate nothing.
+ *
+ * Layout: rows are packed back to back.  Image b's rows start at
+ * sum_{b' < b} N[b'] in X, X_pre, X_post (and the score outputs), and its
+ * kept entries start at sum_{b' < b} K[b'] in out, out_idx, out_src.
+ * Row widths: X and out have D elements, X_pre and X_post have Dc.
+ *
+ * Asynchrony: work is enqueued on `stream` (a hipStream_t; NULL = the null
+ * stream) and the call returns before it completes.  Buffers must stay valid
+ * until the stream reaches that point.  A context must not be used by two
+ * threads or two streams at once (its scratch is shared); distinct contexts
+ * are independent.
+ *
+ * Errors: argument and capacity errors return TR_EINVAL (or TR_EUNSUPPORTED)
+ * synchronously with nothing enqueued.  TR_EDEVICE reports a HIP failure at
+ * launch.  tr_last_error gives a one-line description of the latest failure.
+ */
+#ifndef TR_H
+#define TR_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct tr_ctx tr_ctx;
+
+typedef enum {
+    TR_OK = 0,
+    TR_EINVAL = 1,        /* bad argument, size or capacity                   */
+    TR_ENOMEM = 2,        /* device or host allocation failed in tr_create    */
+    TR_EUNSUPPORTED = 3,  /* valid request this build cannot serve            */
+    TR_EDEVICE = 4        /* HIP runtime error                                */
+} tr_status;
+
+typedef enum {
+    TR_FP32 = 0,          /* IEEE binary32 elements                           */
+    TR_BF16 = 1           /* bfloat16 elements (upper half of a binary32)     */
+} tr_dtype;
+
+/* Problem statement and capacities, fixed for the life of a context. */
+typedef struct {
+    int32_t D;            /* elements per row of X and out (> 0)                   */
+    int32_t Dc;           /* elements per row of X_pre / X_post; 0 means D          */
+    int32_t dtype;        /* tr_dtype of X, X_pre, X_post and out                  */
+    int32_t max_images;   /* largest B accepted by tr_reduce / tr_select (>= 1)     */
+    int64_t max_tokens;   /* largest sum of N[b] accepted (>= 1, < 2^31)            */
+    int32_t max_N;        /* largest single N[b] accepted (>= 1)                    */
+    int32_t reserved;     /* must be 0                                              */
+    double lambda;        /* balance factor in [0, 1] (Algorithm 1; the paper's
+                             efficiency setting is 1/3: 64 + 128 of 192)            */
+    double keep_ratio;    /* used when K == NULL: K_b = clamp(floor(keep_ratio N_b),
+                             1, N_b); must be in (0, 1] if used, else ignored      */
+} tr_params;
+
+/* Create a context on the current HIP device: validates p, allocates scratch
+ * for max_tokens tokens (12 bytes each) and checks that max_N fits the
+ * per-image selection's on-chip memory.  Returns TR_EINVAL for a bad field,
+ * TR_EUNSUPPORTED when max_N exceeds the selection capacity (tr_capacity_N),
+ * TR_ENOMEM or TR_EDEVICE on runtime failure.  *out is NULL on failure. */
+tr_status tr_create(const tr_params* p, tr_ctx** out);
+
+/* The whole module (steps 1-7 above) on a packed batch of B images.
+ *   X      device [sum N, D]   tokens scored by Eq. (3)-(4) and gathered
+ *   X_pre  device [sum N, Dc]  pre-MLP states x'  (Eq. 5-6)
+ *   X_post device [sum N, Dc]  post-MLP states x'' (Eq. 5-6)
+ *   B      number of images, 0 <= B <= max_images (B = 0 is a no-op)
+ *   N      host [B], 1 <= N[b] <= max_N, sum N <= max_tokens
+ *   K      host [B] with 1 <= K[b] <= N[b], or NULL to use keep_ratio
+ *   out    device [sum K, D]   kept rows of X, byte copies, ascending index
+ *   out_idx device int32 [sum K] kept token indices, image-local, strictly
+ *          ascending within an image
+ *   out_src device uint8 [sum K] or NULL: 0 = kept by Stage I, 1 = Stage II
+ *   out_h2 device float [sum N] or NULL: H2 of every token (nats)
+ *   out_s  device float [sum N] or NULL: s of every token
+ *   stream hipStream_t or NULL
+ * X, X_pre, X_post and out may have any alignment (16-byte aligned bases and
+ * row pitches take the vector path; others a scalar path with bit-identical
+ * results). */
+tr_status tr_reduce(tr_ctx* ctx, const void* X, const void* X_pre,
+                    const void* X_post, int32_t B, const int32_t* N,
+                    const int32_t* K, void* out, int32_t* out_idx,
+                    uint8_t* out_src, float* out_h2, float* out_s,
+                    void* stream);
+
+/* Step 2 and step 4 alone (Eq. 3-4 and Eq. 6) over `rows` packed rows, with
+ * the same kernel and bit-identical results as inside tr_reduce.
+ *   key_imp device float [rows]: the Stage I key CV^2 = Var|x| / mean|x|^2
+ *           (population variance over the D channels), D - 1 for an all-zero
+ *           row; ascending CV^2 is descending H2
+ *   key_s   device float [rows]: s (Eq. 6)
+ *   out_h2  device float [rows] or NULL: H2 = log D - log1p(CV^2)
+ * rows may be any value >= 0 (no capacity applies). */
+tr_status tr_score(tr_ctx* ctx, const void* X, const void* X_pre,
+                   const void* X_post, int64_t rows, float* key_imp,
+                   float* key_s, float* out_h2, void* stream);
+
+/* Steps 1, 3, 5, 6 and 7 (without the row gather) from given per-token keys:
+ * the same selection tr_reduce runs, for callers that already hold scores.
+ *   key_imp device float [sum N]: Stage I key, SMALLER is more important
+ *           (tr_reduce uses CV^2; -H2 gives the same order)
+ *   key_s   device float [sum N]: Stage II key (s), sorted ascending
+ *   B, N, K as in tr_reduce; out_idx, out_src as in tr_reduce.
+ * Keys are compared as IEEE values (-0 == +0); ties resolve by index.  NaN
+ * keys give unspecified (memory-safe) order. */
+tr_status tr_select(tr_ctx* ctx, const float* key_imp, const float* key_s,
+                    int32_t B, const int32_t* N, const int32_t* K,
+                    int32_t* out_idx, uint8_t* out_src, void* stream);
+
+/* Host-only budget plan (Algorithm 1, step 1 and the stride of step 6) with
+ * the same validation tr_reduce applies; needs no device.  p may carry zero
+ * capacities (then only the per-image rules are checked).  For each image
+ * writes the kept count, K1, K2 and the stride t (0 when K2 = 0) into the
+ * optional host arrays Kout, K1out, K2out, tout (each [B] or NULL). */
+tr_status tr_plan(const tr_params* p, int32_t B, const int32_t* N,
+                  const int32_t* K, int32_t* Kout, int32_t* K1out,
+                  int32_t* K2out, int32_t* tout);
+
+/* Largest N a context on the current device can select in on-chip memory. */
+int32_t tr_capacity_N(void);
+
+/* Per-stage kernel timing for measurement: when enabled, tr_reduce records
+ * HIP events around its score, select and gather kernels on the caller's
+ * stream.  tr_timing_read waits for the recorded calls, writes the summed
+ * milliseconds of each stage into ms[3] (score, select, gather) and the
+ * number of calls into *calls, then clears the record.  At most 1024 calls
+ * are kept between reads (later calls are not timed). */
+tr_status tr_timing_enable(tr_ctx* ctx, int32_t enable);
+tr_status tr_timing_read(tr_ctx* ctx, double* ms, int64_t* calls);
+
+/* Release the context and its scratch (NULL is a no-op).  Freeing device
+ * memory waits for the device to finish outstanding work first. */
+void tr_destroy(tr_ctx* ctx);
+
+/* Static description of a status code. */
+const char* tr_strerror(tr_status s);
+
+/* One-line description of the latest failure in this thread ("" if none). */
+const char* tr_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TR_H */

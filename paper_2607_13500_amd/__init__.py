@@ -1,0 +1,223 @@
+"""MI355X-native ALTR visual-token reduction (Python binding of include/tr.h).
+
+Every step of the path runs in the HIP library libaltr.so (gfx950):
+
+* score  - Eq. (3)-(4) Renyi-2 entropy and Eq. (6) MLP-consistency cosine,
+           one HBM pass, one wavefront per token;
+* select - Algorithm 1: top-K1 by entropy, ascending sort of the remainder by
+           the cosine, stride picks, union in token order (LDS-resident);
+* gather - byte copies of the kept rows into a compact [sum K, D] output.
+
+This module only marshals torch tensors (device memory) and the current torch
+stream into the C ABI; it computes nothing itself.  If the library is missing
+or the tensors are not on a ROCm device, calls raise.
+"""
+from __future__ import annotations
+
+import ctypes
+from typing import NamedTuple, Optional, Sequence
+
+import torch
+
+from . import _lib
+from ._lib import Params
+
+__all__ = ["Reducer", "ReduceResult", "TRError", "plan", "capacity_N", "LAMBDA_PAPER"]
+
+LAMBDA_PAPER = 1.0 / 3.0   # 64 importance + 128 diversity of 192 (efficiency setting)
+
+_DTYPES = {torch.float32: _lib.TR_FP32, torch.bfloat16: _lib.TR_BF16}
+
+
+class TRError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        lib = _lib.load()
+        msg = lib.tr_last_error().decode() or lib.tr_strerror(status).decode()
+        super().__init__("%s failed (%s): %s" % (where, lib.tr_strerror(status).decode(), msg))
+        self.status = status
+
+
+def _check(status: int, where: str):
+    if status != _lib.TR_OK:
+        raise TRError(status, where)
+
+
+def _i32(seq) -> ctypes.Array:
+    arr = (ctypes.c_int32 * len(seq))(*[int(v) for v in seq])
+    return arr
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _params(D, Dc, dtype, lam, keep_ratio, max_images, max_tokens, max_N) -> Params:
+    if dtype not in _DTYPES:
+        raise TypeError("dtype must be torch.float32 or torch.bfloat16")
+    return Params(D=int(D), Dc=int(Dc or 0), dtype=_DTYPES[dtype], max_images=int(max_images),
+                  max_tokens=int(max_tokens), max_N=int(max_N), reserved=0, lam=float(lam),
+                  keep_ratio=float(keep_ratio or 0.0))
+
+
+def plan(N: Sequence[int], K: Optional[Sequence[int]] = None, lam: float = LAMBDA_PAPER,
+         keep_ratio: Optional[float] = None):
+    """Host-only budget plan of the library: lists (K, K1, K2, t) per image."""
+    lib = _lib.load()
+    B = len(N)
+    p = _params(1, 0, torch.float32, lam, keep_ratio, 0, 0, 0)
+    outs = [(ctypes.c_int32 * max(B, 1))() for _ in range(4)]
+    st = lib.tr_plan(ctypes.byref(p), B, _i32(N), None if K is None else _i32(K), *outs)
+    _check(st, "tr_plan")
+    return tuple([list(o[:B]) for o in outs])
+
+
+def capacity_N() -> int:
+    """Largest per-image N the selection handles on the current device."""
+    return int(_lib.load().tr_capacity_N())
+
+
+class ReduceResult(NamedTuple):
+    out: torch.Tensor              # [sum K, D] kept rows of X
+    idx: torch.Tensor              # [sum K] int32, image-local, ascending per image
+    src: Optional[torch.Tensor]    # [sum K] uint8, 0 = Stage I, 1 = Stage II
+    h2: Optional[torch.Tensor]     # [sum N] float32
+    s: Optional[torch.Tensor]      # [sum N] float32
+
+
+class Reducer:
+    """A library context bound to one device, row widths, dtype and lambda."""
+
+    def __init__(self, D: int, Dc: Optional[int] = None, dtype: torch.dtype = torch.bfloat16,
+                 lam: float = LAMBDA_PAPER, keep_ratio: Optional[float] = None,
+                 max_images: int = 256, max_tokens: int = 1 << 20, max_N: Optional[int] = None,
+                 device=None):
+        if not torch.cuda.is_available():
+            raise RuntimeError("paper_2607_13500_amd needs a ROCm GPU (gfx950)")
+        self.device = torch.device("cuda", torch.cuda.current_device() if device is None
+                                   else torch.device(device).index or 0)
+        self.lib = _lib.load()
+        self.D, self.Dc, self.dtype = int(D), int(Dc or D), dtype
+        self.lam, self.keep_ratio = float(lam), keep_ratio
+        if max_N is None:
+            max_N = min(capacity_N_on(self.device), int(max_tokens))
+        self.max_images, self.max_tokens, self.max_N = int(max_images), int(max_tokens), int(max_N)
+        p = _params(D, Dc, dtype, lam, keep_ratio, max_images, max_tokens, max_N)
+        ctx = ctypes.c_void_p()
+        with torch.cuda.device(self.device):
+            _check(self.lib.tr_create(ctypes.byref(p), ctypes.byref(ctx)), "tr_create")
+        self._ctx = ctx
+
+    # -- helpers ----------------------------------------------------------
+    def _stream(self, stream):
+        st = stream if stream is not None else torch.cuda.current_stream(self.device)
+        return ctypes.c_void_p(st.cuda_stream)
+
+    def _check_rows(self, name, t, width):
+        if not isinstance(t, torch.Tensor) or t.device != self.device:
+            raise ValueError("%s must be a tensor on %s" % (name, self.device))
+        if t.dtype != self.dtype:
+            raise TypeError("%s must be %s, got %s" % (name, self.dtype, t.dtype))
+        if t.dim() != 2 or t.shape[1] != width or not t.is_contiguous():
+            raise ValueError("%s must be a contiguous [rows, %d] tensor, got %s"
+                             % (name, width, tuple(t.shape)))
+
+    def kept_counts(self, N: Sequence[int], K: Optional[Sequence[int]] = None):
+        Kb, _, _, _ = plan(N, K, self.lam, self.keep_ratio)
+        return Kb
+
+    # -- the module ---------------------------------------------------------
+    def reduce(self, X: torch.Tensor, Xpre: torch.Tensor, Xpost: torch.Tensor,
+               N: Sequence[int], K: Optional[Sequence[int]] = None, *,
+               out: Optional[torch.Tensor] = None, out_idx: Optional[torch.Tensor] = None,
+               out_src: Optional[torch.Tensor] = None, want_src: bool = True,
+               want_scores: bool = False, stream=None) -> ReduceResult:
+        """Run score -> select -> gather on a packed batch (asynchronous)."""
+        self._check_rows("X", X, self.D)
+        self._check_rows("Xpre", Xpre, self.Dc)
+        self._check_rows("Xpost", Xpost, self.Dc)
+        rows = X.shape[0]
+        if Xpre.shape[0] != rows or Xpost.shape[0] != rows or sum(int(n) for n in N) != rows:
+            raise ValueError("X, Xpre, Xpost must have sum(N) = %d rows" % sum(int(n) for n in N))
+        sk = sum(self.kept_counts(N, K)) if len(N) else 0
+        dev = self.device
+        if out is None:
+            out = torch.empty(sk, self.D, dtype=self.dtype, device=dev)
+        if out_idx is None:
+            out_idx = torch.empty(sk, dtype=torch.int32, device=dev)
+        if out_src is None and want_src:
+            out_src = torch.empty(sk, dtype=torch.uint8, device=dev)
+        h2 = torch.empty(rows, dtype=torch.float32, device=dev) if want_scores else None
+        s = torch.empty(rows, dtype=torch.float32, device=dev) if want_scores else None
+        for name, t, shape, dt in (("out", out, (sk, self.D), self.dtype),
+                                   ("out_idx", out_idx, (sk,), torch.int32),
+                                   ("out_src", out_src, (sk,), torch.uint8)):
+            if t is not None and (t.device != dev or tuple(t.shape) != shape or t.dtype != dt
+                                  or not t.is_contiguous()):
+                raise ValueError("%s must be a contiguous %s tensor of shape %s on %s"
+                                 % (name, dt, shape, dev))
+        st = self.lib.tr_reduce(self._ctx, _ptr(X), _ptr(Xpre), _ptr(Xpost), len(N), _i32(N),
+                                None if K is None else _i32(K), _ptr(out), _ptr(out_idx),
+                                _ptr(out_src), _ptr(h2), _ptr(s), self._stream(stream))
+        _check(st, "tr_reduce")
+        return ReduceResult(out, out_idx, out_src, h2, s)
+
+    def score(self, X: torch.Tensor, Xpre: torch.Tensor, Xpost: torch.Tensor, *,
+              want_h2: bool = False, stream=None):
+        """Scoring kernel alone: (CV^2 key, s, H2 or None), float32 [rows] each."""
+        self._check_rows("X", X, self.D)
+        self._check_rows("Xpre", Xpre, self.Dc)
+        self._check_rows("Xpost", Xpost, self.Dc)
+        rows = X.shape[0]
+        if Xpre.shape[0] != rows or Xpost.shape[0] != rows:
+            raise ValueError("X, Xpre and Xpost must have the same number of rows")
+        f32 = dict(dtype=torch.float32, device=self.device)
+        cv2, s = torch.empty(rows, **f32), torch.empty(rows, **f32)
+        h2 = torch.empty(rows, **f32) if want_h2 else None
+        st = self.lib.tr_score(self._ctx, _ptr(X), _ptr(Xpre), _ptr(Xpost), rows, _ptr(cv2),
+                               _ptr(s), _ptr(h2), self._stream(stream))
+        _check(st, "tr_score")
+        return cv2, s, h2
+
+    def select(self, key_imp: torch.Tensor, key_s: torch.Tensor, N: Sequence[int],
+               K: Optional[Sequence[int]] = None, *, want_src: bool = True, stream=None):
+        """Algorithm 1 selection from given fp32 keys (Stage I key: smaller first)."""
+        for name, t in (("key_imp", key_imp), ("key_s", key_s)):
+            if t.device != self.device or t.dtype != torch.float32 or t.dim() != 1 \
+                    or not t.is_contiguous() or t.numel() != sum(int(n) for n in N):
+                raise ValueError("%s must be a contiguous float32 [sum N] tensor on %s"
+                                 % (name, self.device))
+        sk = sum(self.kept_counts(N, K)) if len(N) else 0
+        idx = torch.empty(sk, dtype=torch.int32, device=self.device)
+        src = torch.empty(sk, dtype=torch.uint8, device=self.device) if want_src else None
+        st = self.lib.tr_select(self._ctx, _ptr(key_imp), _ptr(key_s), len(N), _i32(N),
+                                None if K is None else _i32(K), _ptr(idx), _ptr(src),
+                                self._stream(stream))
+        _check(st, "tr_select")
+        return idx, src
+
+    # -- measurement --------------------------------------------------------
+    def timing(self, enable: bool = True):
+        _check(self.lib.tr_timing_enable(self._ctx, 1 if enable else 0), "tr_timing_enable")
+
+    def timing_read(self):
+        """(ms per stage [score, select, gather] summed over calls, calls)."""
+        ms = (ctypes.c_double * 3)()
+        calls = ctypes.c_int64()
+        _check(self.lib.tr_timing_read(self._ctx, ms, ctypes.byref(calls)), "tr_timing_read")
+        return list(ms), int(calls.value)
+
+    def close(self):
+        if getattr(self, "_ctx", None):
+            self.lib.tr_destroy(self._ctx)
+            self._ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def capacity_N_on(device) -> int:
+    with torch.cuda.device(device):
+        return capacity_N()

@@ -1,0 +1,489 @@
+// Host runtime behind the C ABI of include/tr.h: validation, budget plan
+// (Algorithm 1), scratch ownership, launch orchestration and timing.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <new>
+#include <string>
+#include <vector>
+
+#include "tr.h"
+#include "tr_internal.h"
+
+using tr::ImageDesc;
+
+namespace {
+
+thread_local std::string g_err;
+
+tr_status fail(tr_status st, const char* fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return st;
+}
+
+tr_status hip_fail(hipError_t e, const char* what)
+{
+    return fail(TR_EDEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+constexpr int kTimedCalls = 1024;
+constexpr int kLdsFallback = 65536;
+
+int elem_bytes(int32_t dtype) { return dtype == TR_BF16 ? 2 : 4; }
+
+// Checks of the problem statement shared by tr_create and tr_plan.
+tr_status check_params(const tr_params* p, bool need_caps)
+{
+    if (!p) return fail(TR_EINVAL, "params is NULL");
+    if (p->D <= 0) return fail(TR_EINVAL, "D must be > 0 (got %d)", p->D);
+    if (p->Dc < 0) return fail(TR_EINVAL, "Dc must be >= 0 (got %d)", p->Dc);
+    if (p->dtype != TR_FP32 && p->dtype != TR_BF16)
+        return fail(TR_EINVAL, "dtype must be TR_FP32 or TR_BF16 (got %d)", p->dtype);
+    if (p->reserved != 0) return fail(TR_EINVAL, "reserved field must be 0");
+    if (!(p->lambda >= 0.0 && p->lambda <= 1.0))
+        return fail(TR_EINVAL, "lambda must be in [0, 1] (got %g)", p->lambda);
+    if (!(p->keep_ratio == 0.0 || (p->keep_ratio > 0.0 && p->keep_ratio <= 1.0)))
+        return fail(TR_EINVAL, "keep_ratio must be 0 (unused) or in (0, 1] (got %g)", p->keep_ratio);
+    const int64_t eb = elem_bytes(p->dtype);
+    const int64_t dc = p->Dc ? p->Dc : p->D;
+    if ((int64_t)p->D * eb > (int64_t)INT32_MAX || dc * eb > (int64_t)INT32_MAX)
+        return fail(TR_EINVAL, "row too wide");
+    if (need_caps) {
+        if (p->max_images < 1) return fail(TR_EINVAL, "max_images must be >= 1");
+        if (p->max_tokens < 1 || p->max_tokens > (int64_t)INT32_MAX)
+            return fail(TR_EINVAL, "max_tokens must be in [1, 2^31 - 1]");
+        if (p->max_N < 1) return fail(TR_EINVAL, "max_N must be >= 1");
+    }
+    return TR_OK;
+}
+
+struct Plan {
+    std::vector<ImageDesc> desc;
+    int64_t sum_n = 0;
+    int64_t sum_k = 0;
+    int nmax = 0;
+    bool uniform = true;
+};
+
+// Algorithm 1, step 1 (K1 = floor(lambda K) in double, K2 = K - K1) and the
+// stride t = max(1, floor((N - K1) / K2)), with every per-image check.
+tr_status make_plan(const tr_params* p, int32_t B, const int32_t* N, const int32_t* K, Plan& out)
+{
+    if (B < 0) return fail(TR_EINVAL, "B must be >= 0 (got %d)", B);
+    if (p->max_images > 0 && B > p->max_images)
+        return fail(TR_EINVAL, "B = %d exceeds max_images = %d", B, p->max_images);
+    if (B > 0 && !N) return fail(TR_EINVAL, "N is NULL");
+    if (B > 0 && !K && !(p->keep_ratio > 0.0))
+        return fail(TR_EINVAL, "K is NULL and no keep_ratio was set");
+    out.desc.resize((size_t)B);
+    int64_t rows = 0, outs = 0;
+    for (int32_t b = 0; b < B; ++b) {
+        const int32_t n = N[b];
+        if (n < 1) return fail(TR_EINVAL, "N[%d] = %d must be >= 1", b, n);
+        if (n > 65535) return fail(TR_EINVAL, "N[%d] = %d exceeds 65535", b, n);
+        if (p->max_N > 0 && n > p->max_N)
+            return fail(TR_EINVAL, "N[%d] = %d exceeds max_N = %d", b, n, p->max_N);
+        int32_t k;
+        if (K) {
+            k = K[b];
+        } else {
+            const double kr = floor(p->keep_ratio * (double)n);
+            k = kr < 1.0 ? 1 : (kr > (double)n ? n : (int32_t)kr);
+        }
+        if (k < 1 || k > n) return fail(TR_EINVAL, "K[%d] = %d must be in [1, N = %d]", b, k, n);
+        const int32_t k1 = (int32_t)floor(p->lambda * (double)k);
+        const int32_t k2 = k - k1;
+        int32_t t = 0;
+        if (k2 > 0) {
+            t = (n - k1) / k2;
+            if (t < 1) t = 1;
+        }
+        ImageDesc& d = out.desc[(size_t)b];
+        d.row_off = (int32_t)rows;
+        d.n = n;
+        d.k1 = k1;
+        d.k2 = k2;
+        d.t = t;
+        d.out_off = (int32_t)outs;
+        rows += n;
+        outs += k;
+        if (rows > (int64_t)INT32_MAX) return fail(TR_EINVAL, "sum of N exceeds 2^31 - 1");
+        if (n > out.nmax) out.nmax = n;
+        if (b > 0) {
+            const ImageDesc& d0 = out.desc[0];
+            if (d.n != d0.n || d.k1 != d0.k1 || d.k2 != d0.k2) out.uniform = false;
+        }
+    }
+    if (p->max_tokens > 0 && rows > p->max_tokens)
+        return fail(TR_EINVAL, "sum of N = %lld exceeds max_tokens = %lld", (long long)rows,
+                    (long long)p->max_tokens);
+    out.sum_n = rows;
+    out.sum_k = outs;
+    return TR_OK;
+}
+
+int lds_limit_of(int dev)
+{
+    int v = 0;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess || v <= 0)
+        v = kLdsFallback;
+    return v;
+}
+
+int capacity_for(int lds_limit)
+{
+    int lo = 0, hi = 65535;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) / 2;
+        if (tr::select_lds_bytes(mid, tr::select_threads(mid)) <= (size_t)lds_limit) lo = mid;
+        else hi = mid - 1;
+    }
+    return lo;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+struct DeviceGuard {
+    int prev = -1;
+    bool ok = true;
+    explicit DeviceGuard(int dev)
+    {
+        if (hipGetDevice(&prev) != hipSuccess) prev = -1;
+        if (prev != dev) ok = hipSetDevice(dev) == hipSuccess;
+    }
+    ~DeviceGuard()
+    {
+        int cur = -1;
+        if (prev >= 0 && hipGetDevice(&cur) == hipSuccess && cur != prev) (void)hipSetDevice(prev);
+    }
+};
+
+}  // namespace
+
+struct tr_ctx {
+    tr_params p{};
+    int device = 0;
+    int Dc = 0;
+    int eb = 4;
+    int lds_limit = 0;
+    int cap_n = 0;
+    float* key_imp = nullptr;
+    float* key_s = nullptr;
+    int32_t* rows = nullptr;
+    bool timing = false;
+    std::vector<hipEvent_t> events;   // 4 per timed call
+    int timed = 0;
+    int64_t untimed = 0;
+};
+
+namespace {
+
+// Launch the selection for every image of a plan (one launch when the batch is
+// uniform, else groups of at most kMaxDescPerLaunch images).
+hipError_t run_select(const Plan& pl, const float* key_imp, const float* key_s, int32_t* out_idx,
+                      uint8_t* out_src, int32_t* out_rows, hipStream_t s)
+{
+    tr::SelectArgs a;
+    memset(&a, 0, sizeof a);
+    a.key_imp = key_imp;
+    a.key_s = key_s;
+    a.out_idx = out_idx;
+    a.out_src = out_src;
+    a.out_rows = out_rows;
+    const int B = (int)pl.desc.size();
+    if (B == 0) return hipSuccess;
+    if (pl.uniform) {
+        a.uniform = 1;
+        a.nimg = B;
+        a.img0 = 0;
+        a.desc[0] = pl.desc[0];
+        return tr::launch_select(a, pl.nmax, s);
+    }
+    for (int b0 = 0; b0 < B; b0 += tr::kMaxDescPerLaunch) {
+        const int nb = B - b0 < tr::kMaxDescPerLaunch ? B - b0 : tr::kMaxDescPerLaunch;
+        a.uniform = 0;
+        a.nimg = nb;
+        a.img0 = b0;
+        int nmax = 0;
+        for (int i = 0; i < nb; ++i) {
+            a.desc[i] = pl.desc[(size_t)(b0 + i)];
+            if (a.desc[i].n > nmax) nmax = a.desc[i].n;
+        }
+        hipError_t e = tr::launch_select(a, nmax, s);
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+tr_status check_ctx_plan(tr_ctx* c, int32_t B, const int32_t* N, const int32_t* K, Plan& pl)
+{
+    tr_status st = make_plan(&c->p, B, N, K, pl);
+    if (st != TR_OK) return st;
+    if (pl.nmax > c->cap_n)
+        return fail(TR_EUNSUPPORTED, "N = %d exceeds the selection capacity %d", pl.nmax, c->cap_n);
+    return TR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* tr_strerror(tr_status s)
+{
+    switch (s) {
+    case TR_OK: return "success";
+    case TR_EINVAL: return "invalid argument";
+    case TR_ENOMEM: return "out of memory";
+    case TR_EUNSUPPORTED: return "unsupported request";
+    case TR_EDEVICE: return "HIP device error";
+    }
+    return "unknown status";
+}
+
+const char* tr_last_error(void) { return g_err.c_str(); }
+
+int32_t tr_capacity_N(void)
+{
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 0;
+    return capacity_for(lds_limit_of(dev));
+}
+
+tr_status tr_plan(const tr_params* p, int32_t B, const int32_t* N, const int32_t* K, int32_t* Kout,
+                  int32_t* K1out, int32_t* K2out, int32_t* tout)
+{
+    g_err.clear();
+    tr_status st = check_params(p, false);
+    if (st != TR_OK) return st;
+    Plan pl;
+    st = make_plan(p, B, N, K, pl);
+    if (st != TR_OK) return st;
+    for (int32_t b = 0; b < B; ++b) {
+        const ImageDesc& d = pl.desc[(size_t)b];
+        if (Kout) Kout[b] = d.k1 + d.k2;
+        if (K1out) K1out[b] = d.k1;
+        if (K2out) K2out[b] = d.k2;
+        if (tout) tout[b] = d.t;
+    }
+    return TR_OK;
+}
+
+tr_status tr_create(const tr_params* p, tr_ctx** out)
+{
+    g_err.clear();
+    if (!out) return fail(TR_EINVAL, "out is NULL");
+    *out = nullptr;
+    tr_status st = check_params(p, true);
+    if (st != TR_OK) return st;
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    const int lds = lds_limit_of(dev);
+    const int cap = capacity_for(lds);
+    if (p->max_N > cap)
+        return fail(TR_EUNSUPPORTED, "max_N = %d exceeds the selection capacity %d of this device",
+                    p->max_N, cap);
+    tr_ctx* c = new (std::nothrow) tr_ctx;
+    if (!c) return fail(TR_ENOMEM, "host allocation failed");
+    c->p = *p;
+    c->device = dev;
+    c->Dc = p->Dc ? p->Dc : p->D;
+    c->eb = elem_bytes(p->dtype);
+    c->lds_limit = lds;
+    c->cap_n = cap;
+    const size_t n = (size_t)p->max_tokens;
+    if ((e = hipMalloc(&c->key_imp, n * sizeof(float))) != hipSuccess ||
+        (e = hipMalloc(&c->key_s, n * sizeof(float))) != hipSuccess ||
+        (e = hipMalloc(&c->rows, n * sizeof(int32_t))) != hipSuccess) {
+        tr_destroy(c);
+        return fail(TR_ENOMEM, "hipMalloc of %zu-token scratch failed: %s", n, hipGetErrorString(e));
+    }
+    if ((e = tr::select_prepare(lds)) != hipSuccess) {
+        tr_destroy(c);
+        return hip_fail(e, "hipFuncSetAttribute");
+    }
+    *out = c;
+    return TR_OK;
+}
+
+void tr_destroy(tr_ctx* c)
+{
+    if (!c) return;
+    DeviceGuard g(c->device);
+    if (c->key_imp) (void)hipFree(c->key_imp);
+    if (c->key_s) (void)hipFree(c->key_s);
+    if (c->rows) (void)hipFree(c->rows);
+    for (hipEvent_t ev : c->events) (void)hipEventDestroy(ev);
+    delete c;
+}
+
+tr_status tr_timing_enable(tr_ctx* c, int32_t enable)
+{
+    g_err.clear();
+    if (!c) return fail(TR_EINVAL, "ctx is NULL");
+    DeviceGuard g(c->device);
+    if (enable && c->events.empty()) {
+        c->events.resize((size_t)kTimedCalls * 4, nullptr);
+        for (hipEvent_t& ev : c->events) {
+            hipError_t e = hipEventCreate(&ev);
+            if (e != hipSuccess) return hip_fail(e, "hipEventCreate");
+        }
+    }
+    c->timing = enable != 0;
+    c->timed = 0;
+    c->untimed = 0;
+    return TR_OK;
+}
+
+tr_status tr_timing_read(tr_ctx* c, double* ms, int64_t* calls)
+{
+    g_err.clear();
+    if (!c || !ms) return fail(TR_EINVAL, "ctx or ms is NULL");
+    DeviceGuard g(c->device);
+    double acc[3] = {0, 0, 0};
+    for (int i = 0; i < c->timed; ++i) {
+        hipEvent_t* ev = &c->events[(size_t)i * 4];
+        hipError_t e = hipEventSynchronize(ev[3]);
+        if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+        for (int k = 0; k < 3; ++k) {
+            float t = 0.f;
+            e = hipEventElapsedTime(&t, ev[k], ev[k + 1]);
+            if (e != hipSuccess) return hip_fail(e, "hipEventElapsedTime");
+            acc[k] += t;
+        }
+    }
+    ms[0] = acc[0];
+    ms[1] = acc[1];
+    ms[2] = acc[2];
+    if (calls) *calls = c->timed;
+    c->timed = 0;
+    c->untimed = 0;
+    return TR_OK;
+}
+
+tr_status tr_reduce(tr_ctx* c, const void* X, const void* X_pre, const void* X_post, int32_t B,
+                    const int32_t* N, const int32_t* K, void* out, int32_t* out_idx,
+                    uint8_t* out_src, float* out_h2, float* out_s, void* stream)
+{
+    g_err.clear();
+    if (!c) return fail(TR_EINVAL, "ctx is NULL");
+    Plan pl;
+    tr_status st = check_ctx_plan(c, B, N, K, pl);
+    if (st != TR_OK) return st;
+    if (B == 0) return TR_OK;
+    if (!X || !X_pre || !X_post || !out || !out_idx)
+        return fail(TR_EINVAL, "X, X_pre, X_post, out and out_idx must be non-NULL");
+    const uintptr_t em = (uintptr_t)c->eb - 1;
+    if (((uintptr_t)X | (uintptr_t)X_pre | (uintptr_t)X_post | (uintptr_t)out) & em)
+        return fail(TR_EINVAL, "tensor base pointers must be aligned to the element size");
+    if (((uintptr_t)out_idx | (uintptr_t)out_h2 | (uintptr_t)out_s) & 3u)
+        return fail(TR_EINVAL, "out_idx, out_h2 and out_s must be 4-byte aligned");
+
+    const int64_t row_bytes = (int64_t)c->p.D * c->eb;
+    const int64_t rowc_bytes = (int64_t)c->Dc * c->eb;
+    const bool vec_score = aligned16(X) && aligned16(X_pre) && aligned16(X_post) &&
+                           row_bytes % 16 == 0 && rowc_bytes % 16 == 0;
+    const bool vec_gather = aligned16(X) && aligned16(out) && row_bytes % 16 == 0;
+
+    DeviceGuard g(c->device);
+    if (!g.ok) return fail(TR_EDEVICE, "hipSetDevice(%d) failed", c->device);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipEvent_t* ev = nullptr;
+    if (c->timing) {
+        if (c->timed < kTimedCalls) ev = &c->events[(size_t)(c->timed++) * 4];
+        else ++c->untimed;
+    }
+    hipError_t e;
+    if (ev && (e = hipEventRecord(ev[0], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+
+    tr::ScoreArgs sa;
+    sa.X = X;
+    sa.P = X_pre;
+    sa.Q = X_post;
+    sa.rows = pl.sum_n;
+    sa.D = c->p.D;
+    sa.Dc = c->Dc;
+    sa.key_imp = c->key_imp;
+    sa.key_s = c->key_s;
+    sa.out_h2 = out_h2;
+    sa.out_s = out_s;
+    sa.logD = (float)log((double)c->p.D);
+    if ((e = tr::launch_score(sa, c->p.dtype == TR_BF16, vec_score, s)) != hipSuccess)
+        return hip_fail(e, "score kernel launch");
+    if (ev && (e = hipEventRecord(ev[1], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+
+    if ((e = run_select(pl, c->key_imp, c->key_s, out_idx, out_src, c->rows, s)) != hipSuccess)
+        return hip_fail(e, "select kernel launch");
+    if (ev && (e = hipEventRecord(ev[2], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+
+    if ((e = tr::launch_gather(X, out, c->rows, pl.sum_k, pl.sum_n, row_bytes, c->eb, vec_gather, s)) != hipSuccess)
+        return hip_fail(e, "gather kernel launch");
+    if (ev && (e = hipEventRecord(ev[3], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    return TR_OK;
+}
+
+tr_status tr_score(tr_ctx* c, const void* X, const void* X_pre, const void* X_post, int64_t rows,
+                   float* key_imp, float* key_s, float* out_h2, void* stream)
+{
+    g_err.clear();
+    if (!c) return fail(TR_EINVAL, "ctx is NULL");
+    if (rows < 0) return fail(TR_EINVAL, "rows must be >= 0");
+    if (rows == 0) return TR_OK;
+    if (!X || !X_pre || !X_post || !key_imp || !key_s)
+        return fail(TR_EINVAL, "X, X_pre, X_post, key_imp and key_s must be non-NULL");
+    const uintptr_t em = (uintptr_t)c->eb - 1;
+    if (((uintptr_t)X | (uintptr_t)X_pre | (uintptr_t)X_post) & em)
+        return fail(TR_EINVAL, "tensor base pointers must be aligned to the element size");
+    if (((uintptr_t)key_imp | (uintptr_t)key_s | (uintptr_t)out_h2) & 3u)
+        return fail(TR_EINVAL, "score outputs must be 4-byte aligned");
+    const int64_t row_bytes = (int64_t)c->p.D * c->eb;
+    const int64_t rowc_bytes = (int64_t)c->Dc * c->eb;
+    const bool vec = aligned16(X) && aligned16(X_pre) && aligned16(X_post) && row_bytes % 16 == 0 &&
+                     rowc_bytes % 16 == 0;
+    DeviceGuard g(c->device);
+    if (!g.ok) return fail(TR_EDEVICE, "hipSetDevice(%d) failed", c->device);
+    tr::ScoreArgs sa;
+    sa.X = X;
+    sa.P = X_pre;
+    sa.Q = X_post;
+    sa.rows = rows;
+    sa.D = c->p.D;
+    sa.Dc = c->Dc;
+    sa.key_imp = key_imp;
+    sa.key_s = key_s;
+    sa.out_h2 = out_h2;
+    sa.out_s = nullptr;
+    sa.logD = (float)log((double)c->p.D);
+    hipError_t e = tr::launch_score(sa, c->p.dtype == TR_BF16, vec, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "score kernel launch");
+    return TR_OK;
+}
+
+tr_status tr_select(tr_ctx* c, const float* key_imp, const float* key_s, int32_t B, const int32_t* N,
+                    const int32_t* K, int32_t* out_idx, uint8_t* out_src, void* stream)
+{
+    g_err.clear();
+    if (!c) return fail(TR_EINVAL, "ctx is NULL");
+    Plan pl;
+    tr_status st = check_ctx_plan(c, B, N, K, pl);
+    if (st != TR_OK) return st;
+    if (B == 0) return TR_OK;
+    if (!key_imp || !key_s || !out_idx) return fail(TR_EINVAL, "key_imp, key_s and out_idx must be non-NULL");
+    if (((uintptr_t)key_imp | (uintptr_t)key_s | (uintptr_t)out_idx) & 3u)
+        return fail(TR_EINVAL, "key and index arrays must be 4-byte aligned");
+    DeviceGuard g(c->device);
+    if (!g.ok) return fail(TR_EDEVICE, "hipSetDevice(%d) failed", c->device);
+    hipError_t e = run_select(pl, key_imp, key_s, out_idx, out_src, nullptr, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "select kernel launch");
+    return TR_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,70 @@
+// Internal declarations shared by the library's translation units (never by
+// the oracle).  Kernels are launched only from the file that defines them.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace tr {
+
+constexpr int kWave = 64;
+
+// ---- scoring (Eq. 3-4 and Eq. 6, one wavefront per token row) -------------
+struct ScoreArgs {
+    const void* X;       // [rows, D]
+    const void* P;       // [rows, Dc] pre-MLP states
+    const void* Q;       // [rows, Dc] post-MLP states
+    int64_t rows;
+    int32_t D;
+    int32_t Dc;
+    float* key_imp;      // [rows] CV^2 of |x| (Stage I key, ascending)
+    float* key_s;        // [rows] s (Stage II key, ascending)
+    float* out_h2;       // [rows] or nullptr
+    float* out_s;        // [rows] or nullptr
+    float logD;          // log(D) in fp32
+};
+
+// bf16: true for bfloat16 rows, false for fp32.  vec: every row start is
+// 16-byte aligned (vector loads); otherwise element loads with the same
+// per-lane arithmetic order.
+hipError_t launch_score(const ScoreArgs& a, bool bf16, bool vec, hipStream_t s);
+
+// ---- per-image selection (top-K1, ordered remainder, sort, stride) --------
+struct ImageDesc {
+    int32_t row_off;     // first row of the image in the packed batch
+    int32_t n;           // tokens
+    int32_t k1;          // Stage I budget
+    int32_t k2;          // Stage II budget
+    int32_t t;           // stride (>= 1 when k2 > 0)
+    int32_t out_off;     // first output slot
+};
+
+constexpr int kMaxDescPerLaunch = 32;
+
+struct SelectArgs {
+    const float* key_imp;   // packed [sum N]
+    const float* key_s;     // packed [sum N]
+    int32_t* out_idx;       // packed [sum K], image-local
+    uint8_t* out_src;       // packed [sum K] or nullptr
+    int32_t* out_rows;      // packed [sum K] global row of each kept token, or nullptr
+    int32_t uniform;        // 1: desc[0] holds n/k1/k2/t of every image
+    int32_t nimg;           // images in this launch
+    int32_t img0;           // index of the first image (uniform mode)
+    int32_t pad;
+    ImageDesc desc[kMaxDescPerLaunch];
+};
+
+// Threads per selection workgroup for images of at most nmax tokens.
+int select_threads(int nmax);
+// Dynamic LDS bytes the selection needs for an image of n tokens.
+size_t select_lds_bytes(int n, int threads);
+hipError_t select_prepare(int lds_limit);
+hipError_t launch_select(const SelectArgs& a, int nmax, hipStream_t s);
+
+// ---- gather of kept rows ---------------------------------------------------
+// rows[r] outside [0, nrows) are skipped (their output row is left as is).
+hipError_t launch_gather(const void* X, void* out, const int32_t* rows, int64_t nout, int64_t nrows,
+                         int64_t row_bytes, int elem_bytes, bool vec, hipStream_t s);
+
+}  // namespace tr

@@ -1,0 +1,259 @@
+// Fused per-token scoring: one HBM pass over X, X_pre and X_post.
+//
+// One wavefront scores one token row.  The row is cut into chunks of 16 bytes
+// (8 bf16 or 4 fp32 elements); chunk c belongs to lane c % 64 and every lane
+// walks its chunks in ascending c, so a row's arithmetic never depends on
+// where the row sits in the batch (identical rows score identically).
+//
+// Eq. (3)-(4): with m = mean |x| and V = M2 / D (M2 = sum (|x| - m)^2),
+//   sum_j p_j^2 = (1 + V / m^2) / D,  H2 = log D - log1p(CV^2),
+//   CV^2 = M2 / (D m^2).
+// Stage I ranks ascending CV^2 (= descending H2): near-uniform rows have H2
+// within an fp32 ulp of log D but well-separated CV^2.  M2 is accumulated
+// around one shift c shared by the whole row, the mean |x| of its first
+// min(D, 64 * 16 / elem) elements (every lane's first chunk, summed by a
+// butterfly before any other work): d = |x| - c is exact when |x| is within a
+// factor 2 of c (near-uniform rows), and M2 = sum d^2 - (sum d)^2 / D has
+// little cancellation because c lies close to m.
+//
+// Eq. (6): fp32 sums of x'x'', x'^2 and x''^2.
+//
+// Lane partial sums are combined by xor butterflies (every lane ends with the
+// same value) and lane 0 writes the results.
+#include "tr_internal.h"
+
+namespace tr {
+namespace {
+
+// 16 bytes of raw row data.
+struct Raw {
+    uint32_t w[4];
+};
+
+template <bool BF16>
+struct Layout {
+    static constexpr int kV = BF16 ? 8 : 4;    // elements per 16-byte chunk
+    static constexpr int kEB = BF16 ? 2 : 4;   // bytes per element
+};
+
+// bf16 -> fp32 is exact: the stored half is the upper half of the binary32.
+__device__ __forceinline__ float lo_bf16(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float hi_bf16(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+template <bool BF16>
+__device__ __forceinline__ void unpack(const Raw& r, float* v)
+{
+    if constexpr (BF16) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            v[2 * k] = lo_bf16(r.w[k]);
+            v[2 * k + 1] = hi_bf16(r.w[k]);
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) v[k] = __uint_as_float(r.w[k]);
+    }
+}
+
+// Load full chunk c of a row.
+template <bool BF16, bool VEC>
+__device__ __forceinline__ Raw load_chunk(const char* row, int c)
+{
+    Raw r;
+    if constexpr (VEC) {
+        const uint4 q = *reinterpret_cast<const uint4*>(row + (size_t)c * 16);
+        r.w[0] = q.x;
+        r.w[1] = q.y;
+        r.w[2] = q.z;
+        r.w[3] = q.w;
+    } else if constexpr (BF16) {
+        const uint16_t* e = reinterpret_cast<const uint16_t*>(row) + (size_t)c * 8;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) r.w[k] = (uint32_t)e[2 * k] | ((uint32_t)e[2 * k + 1] << 16);
+    } else {
+        const uint32_t* e = reinterpret_cast<const uint32_t*>(row) + (size_t)c * 4;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) r.w[k] = e[k];
+    }
+    return r;
+}
+
+// Load the first m (< kV) elements of chunk c element by element.
+template <bool BF16>
+__device__ __forceinline__ void load_partial(const char* row, int c, int m, float* v)
+{
+    if constexpr (BF16) {
+        const uint16_t* e = reinterpret_cast<const uint16_t*>(row) + (size_t)c * 8;
+        for (int k = 0; k < m; ++k) v[k] = __uint_as_float((uint32_t)e[k] << 16);
+    } else {
+        const float* e = reinterpret_cast<const float*>(row) + (size_t)c * 4;
+        for (int k = 0; k < m; ++k) v[k] = e[k];
+    }
+}
+
+struct XAcc {
+    float sd;    // sum (|x| - c)
+    float sd2;   // sum (|x| - c)^2
+};
+
+struct CAcc {
+    float dot, n1, n2;
+};
+
+__device__ __forceinline__ void x_chunk(XAcc& a, const float* v, int m, float c)
+{
+    for (int k = 0; k < m; ++k) {
+        const float d = fabsf(v[k]) - c;
+        a.sd += d;
+        a.sd2 = fmaf(d, d, a.sd2);
+    }
+}
+
+__device__ __forceinline__ void c_chunk(CAcc& a, const float* p, const float* q, int m)
+{
+    for (int k = 0; k < m; ++k) {
+        a.dot = fmaf(p[k], q[k], a.dot);
+        a.n1 = fmaf(p[k], p[k], a.n1);
+        a.n2 = fmaf(q[k], q[k], a.n2);
+    }
+}
+
+__device__ __forceinline__ float wave_sum(float v)
+{
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) v += __shfl_xor(v, off, kWave);
+    return v;
+}
+
+template <int V>
+__device__ __forceinline__ float abs_sum(const float* v, int m)
+{
+    float s = 0.f;
+    for (int k = 0; k < m; ++k) s += fabsf(v[k]);
+    return s;
+}
+
+template <bool BF16, bool VEC, int UNR>
+__global__ __launch_bounds__(256) void score_kernel(ScoreArgs a)
+{
+    using L = Layout<BF16>;
+    constexpr int V = L::kV;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t row = (int64_t)blockIdx.x * (blockDim.x / kWave) + (threadIdx.x / kWave);
+    if (row >= a.rows) return;   // whole wavefront leaves together
+
+    const char* xr = static_cast<const char*>(a.X) + row * (int64_t)a.D * L::kEB;
+    const char* pr = static_cast<const char*>(a.P) + row * (int64_t)a.Dc * L::kEB;
+    const char* qr = static_cast<const char*>(a.Q) + row * (int64_t)a.Dc * L::kEB;
+    const int nfx = a.D / V;    // full chunks of X
+    const int nfc = a.Dc / V;   // full chunks of X_pre / X_post
+    const int nf = nfx > nfc ? nfx : nfc;
+    // elements in the lanes' first chunks: the sample the shift c averages
+    const float n_probe = (float)(a.D < kWave * V ? a.D : kWave * V);
+
+    // A trailing partial chunk belongs to lane (index % 64) like any other and
+    // is that lane's last chunk.
+    const bool tail_x = (a.D % V) && (nfx & (kWave - 1)) == lane;
+    const int mx = a.D - nfx * V;
+    float tx[V];
+    if (tail_x) load_partial<BF16>(xr, nfx, mx, tx);
+
+    XAcc xa{0.f, 0.f};
+    CAcc ca{0.f, 0.f, 0.f};
+    float c = 0.f;
+    if (nfx == 0) c = wave_sum(tail_x ? abs_sum<V>(tx, mx) : 0.f) / n_probe;
+
+    for (int j0 = 0; j0 < nf; j0 += kWave * UNR) {   // same trip count for every lane
+        Raw rx[UNR], rp[UNR], rq[UNR];
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) {
+            const int ci = j0 + lane + kWave * u;
+            if (ci < nfx) rx[u] = load_chunk<BF16, VEC>(xr, ci);
+            if (ci < nfc) {
+                rp[u] = load_chunk<BF16, VEC>(pr, ci);
+                rq[u] = load_chunk<BF16, VEC>(qr, ci);
+            }
+        }
+        if (j0 == 0 && nfx > 0) {
+            float first = 0.f;
+            if (lane < nfx) {
+                float v[V];
+                unpack<BF16>(rx[0], v);
+                first = abs_sum<V>(v, V);
+            } else if (tail_x) {
+                first = abs_sum<V>(tx, mx);
+            }
+            c = wave_sum(first) / n_probe;
+        }
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) {
+            const int ci = j0 + lane + kWave * u;
+            if (ci < nfx) {
+                float v[V];
+                unpack<BF16>(rx[u], v);
+                x_chunk(xa, v, V, c);
+            }
+            if (ci < nfc) {
+                float p[V], q[V];
+                unpack<BF16>(rp[u], p);
+                unpack<BF16>(rq[u], q);
+                c_chunk(ca, p, q, V);
+            }
+        }
+    }
+    if (tail_x) x_chunk(xa, tx, mx, c);
+    if (a.Dc % V && (nfc & (kWave - 1)) == lane) {
+        float p[V], q[V];
+        const int m = a.Dc - nfc * V;
+        load_partial<BF16>(pr, nfc, m, p);
+        load_partial<BF16>(qr, nfc, m, q);
+        c_chunk(ca, p, q, m);
+    }
+
+    const float sd = wave_sum(xa.sd);
+    const float sd2 = wave_sum(xa.sd2);
+    const float dot = wave_sum(ca.dot);
+    const float n1 = wave_sum(ca.n1);
+    const float n2 = wave_sum(ca.n2);
+
+    if (lane == 0) {
+        const float Df = (float)a.D;
+        const float mean = c + sd / Df;
+        const float m2 = fmaxf(0.f, fmaf(-sd, sd / Df, sd2));
+        float cv2, h2;
+        if (mean > 0.f) {
+            cv2 = (m2 / (mean * Df)) / mean;
+            h2 = a.logD - log1pf(cv2);
+        } else {   // all-zero row: H2 = 0, i.e. 1 + CV^2 = D
+            cv2 = Df - 1.f;
+            h2 = 0.f;
+        }
+        float s = 0.f;
+        if (n1 > 0.f && n2 > 0.f) s = dot / (sqrtf(n1) * sqrtf(n2));
+        a.key_imp[row] = cv2;
+        a.key_s[row] = s;
+        if (a.out_h2) a.out_h2[row] = h2;
+        if (a.out_s) a.out_s[row] = s;
+    }
+}
+
+template <bool BF16, bool VEC>
+hipError_t launch_t(const ScoreArgs& a, hipStream_t s)
+{
+    constexpr int kThreads = 256;
+    constexpr int kRowsPerBlock = kThreads / kWave;
+    const int64_t blocks = (a.rows + kRowsPerBlock - 1) / kRowsPerBlock;
+    if (blocks <= 0) return hipSuccess;
+    hipLaunchKernelGGL((score_kernel<BF16, VEC, 4>), dim3((unsigned)blocks), dim3(kThreads), 0, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_score(const ScoreArgs& a, bool bf16, bool vec, hipStream_t s)
+{
+    if (bf16) return vec ? launch_t<true, true>(a, s) : launch_t<true, false>(a, s);
+    return vec ? launch_t<false, true>(a, s) : launch_t<false, false>(a, s);
+}
+
+}  // namespace tr

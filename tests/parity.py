@@ -1,0 +1,172 @@
+"""Parity protocol between the HIP path and the fp64 oracle.
+
+Scores (fp32 accumulate on the GPU) are compared with the oracle's fp64 values
+within a relative tolerance TOL = 1e-5 (floor 1 for H2 and s, whose natural
+scale is O(1)).  Indices are compared exactly, except where the oracle's own
+score gap is inside the window an fp32 score error of TOL can cross:
+
+* P1  scores: |CV^2_gpu - CV^2| <= TOL CV^2 (+1e-12), |H2_gpu - H2| <=
+      TOL max(1, |H2|), |s_gpu - s| <= TOL max(1, |s|).  CV^2 = expm1(log D - H2)
+      is the quantity the GPU ranks Stage I by (same order as H2).
+* P2  Stage I: the GPU's X^imp may differ from the oracle's only in tokens whose
+      oracle CV^2 lies within 2 TOL of the boundary value (the K1-th smallest);
+      each such token is a counted near-tie swap, anything else fails.
+* P3  Stage II, checked on the GPU's own X^imp so that a P2 swap cannot
+      cascade: order X^rem by the oracle's (s, index); the GPU's j-th pick (in
+      its own s order) must be the token at sorted position j t, or a token
+      whose oracle s is within 2 TOL of it (a counted near tie).
+* P4  output: K kept, strictly ascending, K1 from Stage I and K2 from Stage II,
+      and out equal byte for byte to the kept rows of X.
+* P5  information only: raw mismatch count against the oracle's indices.
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+
+import numpy as np
+import torch
+
+import oracle
+
+TOL = 1e-5
+
+
+@dataclasses.dataclass
+class Report:
+    images: int = 0
+    tokens: int = 0
+    max_rel_cv2: float = 0.0
+    max_abs_h2: float = 0.0
+    max_abs_s: float = 0.0
+    stage1_swaps: int = 0
+    stage1_windows: int = 0
+    stage2_near: int = 0
+    picks: int = 0
+    raw_mismatch: int = 0
+    failures: list = dataclasses.field(default_factory=list)
+
+    def ok(self) -> bool:
+        return not self.failures
+
+    def summary(self) -> str:
+        return ("images=%d tokens=%d max_rel_cv2=%.2e max_abs_h2=%.2e max_abs_s=%.2e "
+                "stage1_swaps=%d (images with a near-tie window: %d) stage2_near=%d/%d picks "
+                "raw_mismatch=%d failures=%d"
+                % (self.images, self.tokens, self.max_rel_cv2, self.max_abs_h2, self.max_abs_s,
+                   self.stage1_swaps, self.stage1_windows, self.stage2_near, self.picks,
+                   self.raw_mismatch, len(self.failures)))
+
+
+def oracle_reference(w, want_out=False):
+    """Run the oracle on CPU copies of a workload (the same bytes the GPU sees)."""
+    return oracle.reduce(w.X.cpu(), w.Xpre.cpu(), w.Xpost.cpu(), w.N, w.K, w.lam,
+                         want_out=want_out, want_scores=True)
+
+
+def cv2_from_h2(h2: np.ndarray, D: int) -> np.ndarray:
+    return np.expm1(math.log(D) - h2)
+
+
+def check(w, res, ref, cv2_gpu=None, tol: float = TOL) -> Report:
+    """Apply P1-P5 to a GPU ReduceResult (with scores) against an oracle run."""
+    rep = Report()
+    D = w.D
+    h2o, so = ref["h2"], ref["s"]
+    cv2o = cv2_from_h2(h2o, D)
+    rep.tokens = h2o.size
+    if res.h2 is not None:
+        h2g = res.h2.double().cpu().numpy()
+        sg = res.s.double().cpu().numpy()
+        dh = np.abs(h2g - h2o)
+        ds = np.abs(sg - so)
+        rep.max_abs_h2 = float(dh.max(initial=0))
+        rep.max_abs_s = float(ds.max(initial=0))
+        bad = np.nonzero(dh > tol * np.maximum(1.0, np.abs(h2o)))[0]
+        if bad.size:
+            rep.failures.append("P1 H2 outside tolerance at rows %s" % bad[:8].tolist())
+        bad = np.nonzero(ds > tol * np.maximum(1.0, np.abs(so)))[0]
+        if bad.size:
+            rep.failures.append("P1 s outside tolerance at rows %s" % bad[:8].tolist())
+    else:
+        sg = None
+    if cv2_gpu is not None:
+        cg = cv2_gpu.double().cpu().numpy()
+        dc = np.abs(cg - cv2o)
+        rel = dc / np.maximum(cv2o, 1e-300)
+        rep.max_rel_cv2 = float(np.where(cv2o > 0, rel, 0).max(initial=0))
+        bad = np.nonzero(dc > tol * cv2o + 1e-12)[0]
+        if bad.size:
+            rep.failures.append("P1 CV^2 outside tolerance at rows %s" % bad[:8].tolist())
+
+    idx_all = res.idx.cpu().numpy()
+    src_all = res.src.cpu().numpy() if res.src is not None else None
+    Xg = w.X
+    r0 = o0 = 0
+    for b, (n, k) in enumerate(zip(w.N, w.K)):
+        K1, K2, t = oracle.budget(n, k, w.lam)
+        idx = idx_all[o0:o0 + k].astype(np.int64)
+        src = src_all[o0:o0 + k]
+        rep.images += 1
+        rep.picks += K2
+        # ---- P4
+        if idx.size != k or (k > 1 and not np.all(np.diff(idx) > 0)) or idx.min() < 0 or idx.max() >= n:
+            rep.failures.append("P4 image %d: indices not %d strictly ascending in [0,%d)" % (b, k, n))
+            r0 += n
+            o0 += k
+            continue
+        if int((src == 0).sum()) != K1 or int((src == 1).sum()) != K2:
+            rep.failures.append("P4 image %d: %d/%d from Stage I/II, want %d/%d"
+                                % (b, (src == 0).sum(), (src == 1).sum(), K1, K2))
+        rows = torch.from_numpy(idx + r0).to(Xg.device)
+        if not torch.equal(res.out[o0:o0 + k].view(torch.int16 if Xg.dtype == torch.bfloat16 else torch.int32),
+                           Xg.index_select(0, rows).view(torch.int16 if Xg.dtype == torch.bfloat16 else torch.int32)):
+            rep.failures.append("P4 image %d: gathered rows differ from X[idx]" % b)
+        # ---- P5
+        ref_idx = ref["idx"][o0:o0 + k]
+        rep.raw_mismatch += k - np.intersect1d(idx, ref_idx).size
+        # ---- P2
+        c = cv2o[r0:r0 + n]
+        imp_g = np.sort(idx[src == 0])
+        imp_o = np.sort(ref_idx[ref["src"][o0:o0 + k] == 0])
+        if K1 > 0:
+            order = np.lexsort((np.arange(n), c))
+            theta = c[order[K1 - 1]]
+            win = 2 * tol * theta + 2e-12
+            if K1 < n and abs(c[order[K1]] - theta) <= win:
+                rep.stage1_windows += 1
+            diff = np.setxor1d(imp_g, imp_o)
+            if diff.size:
+                far = diff[np.abs(c[diff] - theta) > win]
+                if far.size:
+                    rep.failures.append("P2 image %d: Stage I differs beyond near ties at %s"
+                                        % (b, far[:8].tolist()))
+                rep.stage1_swaps += diff.size // 2
+        # ---- P3 (on the GPU's own X^imp)
+        if K2 > 0:
+            s_img = so[r0:r0 + n]
+            in_imp = np.zeros(n, bool)
+            in_imp[imp_g] = True
+            rem = np.nonzero(~in_imp)[0]
+            order = rem[np.lexsort((rem, s_img[rem]))]
+            expect = order[np.arange(K2) * t]
+            div = idx[src == 1]
+            if np.any(in_imp[div]):
+                rep.failures.append("P3 image %d: a Stage II pick is also in X^imp" % b)
+            if sg is not None:
+                sgi = sg[r0:r0 + n]
+                div = div[np.lexsort((div, sgi[div]))]
+            else:
+                div = div[np.lexsort((div, s_img[div]))]
+            mism = np.nonzero(div != expect)[0]
+            if mism.size:
+                gap = np.abs(s_img[div[mism]] - s_img[expect[mism]])
+                lim = 2 * tol * np.maximum(1.0, np.abs(s_img[expect[mism]]))
+                if np.any(gap > lim):
+                    j = mism[np.argmax(gap - lim)]
+                    rep.failures.append("P3 image %d: pick %d is token %d, want %d (s gap %.3e)"
+                                        % (b, j, div[j], expect[j], gap.max()))
+                rep.stage2_near += mism.size
+        r0 += n
+        o0 += k
+    return rep

@@ -1,0 +1,157 @@
+"""CPU checks of the C ABI library: symbols, host budget plan, validation.
+
+Nothing here launches a kernel.  The plan is checked against the budget split
+the paper prints and the keep ratios it runs (tests/golden/).
+"""
+import ctypes
+import os
+import re
+import subprocess
+from fractions import Fraction
+
+import pytest
+
+import paper_2607_13500_amd as tr
+from paper_2607_13500_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+GOLDEN = os.path.join(ROOT, "tests", "golden")
+
+
+def _declared_functions():
+    text = open(os.path.join(ROOT, "include", "tr.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(tr_[a-z_A-Z0-9]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    names = _declared_functions()
+    assert {"tr_create", "tr_reduce", "tr_destroy", "tr_strerror", "tr_score", "tr_select",
+            "tr_plan"} <= set(names)
+    lib = _lib.load()
+    for n in names:
+        assert hasattr(lib, n), n
+    dyn = subprocess.run(["nm", "-D", "--defined-only", _lib.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (tr_\w+)", dyn))
+    assert set(names) <= exported
+    # the product library links the HIP runtime and nothing from the oracle
+    assert "altr_oracle" not in dyn
+
+
+def test_library_built_for_gfx950_only(tmp_path):
+    blob = tmp_path / "fatbin.bin"
+    res = subprocess.run(["objcopy", "-O", "binary", "--only-section=.hip_fatbin", _lib.LIB_PATH,
+                          str(blob)], capture_output=True, text=True)
+    if res.returncode != 0:
+        pytest.skip("objcopy unavailable")
+    targets = set(re.findall(rb"amdgcn-amd-amdhsa--(gfx[0-9a-z]+)", blob.read_bytes()))
+    assert targets == {b"gfx950"}
+
+
+def test_strerror():
+    lib = _lib.load()
+    assert lib.tr_strerror(0) == b"success"
+    assert lib.tr_strerror(1) == b"invalid argument"
+    assert lib.tr_strerror(4) == b"HIP device error"
+    assert lib.tr_strerror(99) == b"unknown status"
+
+
+def _rows(name):
+    out = []
+    for line in open(os.path.join(GOLDEN, name)):
+        line = line.split("#", 1)[0].strip()
+        if line:
+            out.append(line.split())
+    return out
+
+
+def test_plan_matches_golden_budget_split():
+    rows = _rows("budget_split.txt")
+    assert any(r[-1] == "paper" for r in rows)
+    for N, K, ln, ld, K1, K2, t, _ in rows:
+        lam = int(ln) / int(ld)
+        Kb, K1b, K2b, tb = tr.plan([int(N)], [int(K)], lam=lam)
+        assert (Kb[0], K1b[0], K2b[0], tb[0]) == (int(K), int(K1), int(K2), int(t)), (N, K, lam)
+
+
+def test_plan_keep_ratio_matches_paper_budgets():
+    for N, rn, rd, K in _rows("keep_ratio.txt"):
+        ratio = int(rn) / int(rd)
+        Kb, _, _, _ = tr.plan([int(N)], None, keep_ratio=ratio)
+        assert Kb[0] == int(K), (N, ratio)
+
+
+def test_plan_keep_ratio_clamps_and_floors():
+    Kb, K1, K2, t = tr.plan([1, 5, 9, 16384, 256], None, keep_ratio=0.11)
+    assert Kb == [1, 1, 1, 1802, 28]
+    # floor(lambda K) with lambda = 1/3
+    assert K1 == [0, 0, 0, 600, 9]
+    assert all(k1 + k2 == k for k, k1, k2 in zip(Kb, K1, K2))
+    Kb, _, _, _ = tr.plan([7], None, keep_ratio=1.0)
+    assert Kb == [7]
+
+
+def test_plan_budget_exhaustive_small():
+    # Algorithm 1's split and stride over every (N, K, lambda) on a small grid,
+    # checked with exact rational arithmetic (floor of lambda*K for a rational
+    # lambda is exact here because lambda*K is never within 1e-12 of an integer
+    # unless it is one).
+    for N in range(1, 40):
+        for K in range(1, N + 1):
+            for lam in (Fraction(0), Fraction(1, 4), Fraction(1, 3), Fraction(1, 2), Fraction(2, 3),
+                        Fraction(1)):
+                Kb, K1b, K2b, tb = tr.plan([N], [K], lam=float(lam))
+                k1 = (lam * K).numerator // (lam * K).denominator
+                k2 = K - k1
+                t = max(1, (N - k1) // k2) if k2 else 0
+                assert (Kb[0], K1b[0], K2b[0], tb[0]) == (K, k1, k2, t)
+                if k2:
+                    assert (k2 - 1) * t < N - k1     # every pick lands inside X^rem
+
+
+@pytest.mark.parametrize("N,K,kw", [
+    ([0], [1], {}),
+    ([5], [0], {}),
+    ([5], [6], {}),
+    ([5, 7], [2, -1], {}),
+    ([70000], [5], {}),
+    ([5], None, {}),                      # no K and no keep ratio
+    ([5], [2], {"lam": 1.5}),
+    ([5], [2], {"lam": -0.01}),
+    ([5], [2], {"lam": float("nan")}),
+    ([5], None, {"keep_ratio": 1.5}),
+])
+def test_plan_rejects_invalid(N, K, kw):
+    with pytest.raises(tr.TRError) as e:
+        tr.plan(N, K, **kw)
+    assert e.value.status == _lib.TR_EINVAL
+
+
+def test_plan_empty_batch():
+    assert tr.plan([], []) == ([], [], [], [])
+
+
+def test_create_rejects_bad_params_before_touching_a_device():
+    lib = _lib.load()
+    ctx = ctypes.c_void_p()
+    good = dict(D=64, Dc=0, dtype=1, max_images=4, max_tokens=1024, max_N=512, reserved=0,
+                lam=1 / 3, keep_ratio=0.0)
+    bad = [dict(D=0), dict(Dc=-1), dict(dtype=7), dict(max_images=0), dict(max_tokens=0),
+           dict(max_tokens=1 << 31), dict(max_N=0), dict(reserved=1), dict(lam=2.0),
+           dict(keep_ratio=-0.5)]
+    for b in bad:
+        p = _lib.Params(**{**good, **b})
+        assert lib.tr_create(ctypes.byref(p), ctypes.byref(ctx)) == _lib.TR_EINVAL, b
+        assert ctx.value is None
+    assert lib.tr_create(None, ctypes.byref(ctx)) == _lib.TR_EINVAL
+    assert lib.tr_last_error() != b""
+
+
+def test_null_context_calls_are_rejected():
+    lib = _lib.load()
+    N = (ctypes.c_int32 * 1)(4)
+    assert lib.tr_reduce(None, None, None, None, 1, N, None, None, None, None, None, None, None) == _lib.TR_EINVAL
+    assert lib.tr_select(None, None, None, 1, N, None, None, None, None) == _lib.TR_EINVAL
+    assert lib.tr_score(None, None, None, None, 1, None, None, None, None) == _lib.TR_EINVAL
+    lib.tr_destroy(None)
