@@ -36,6 +36,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="target wall time of the oracle sample")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="after the measurement, run 3 plain device copies of this many MiB "
+                         "(the reference dispatch for scaling PMC byte counters)")
     return ap.parse_args()
 
 
@@ -159,6 +162,14 @@ def main():
         line["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
     r.close()
     print(json.dumps(line), flush=True)
+    if args.calib_copy_mib > 0:
+        n = args.calib_copy_mib << 20
+        a = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        print("calibration: 3 device copies of %d bytes" % n, file=sys.stderr, flush=True)
 
 
 if __name__ == "__main__":
