@@ -1,33 +1,95 @@
-// Per-image selection, one workgroup per image, everything resident in LDS.
+// Per-image selection (Algorithm 1 after the scores): one 1024-thread
+// workgroup per image, everything resident in LDS.
 //
-//   Stage I  (top-K1 smallest Stage I key, ties to the lower index):
-//            4-pass MSB-first radix select over order-preserving 32-bit keys
-//            finds the K1-th smallest key T and how many keys equal to T are
-//            taken; an ordered pass then marks keys < T and the first of the
-//            keys == T in index order.
-//   Stage II (X^rem in index order, stable ascending sort by s, stride):
-//            ordered compaction of the unmarked tokens, 4-pass stable LSD radix
-//            sort of their 16-bit indices keyed by s, picks at positions
-//            0, t, ..., (K2-1) t.
-//   Output:  ordered compaction of X^imp U X^div (ascending token index).
+// Keys are fp32 scores mapped to order-preserving u32 (-0 == +0).  Stage I
+// keeps the K1 smallest Stage I keys (ties: lower index); Stage II orders
+// X^rem by the Stage II key (ties: lower index) and keeps sorted positions
+// 0, t, ..., (K2-1) t; the output lists X^imp U X^div in token order.
 //
-// Every wavefront owns a contiguous, 64-aligned range of the array it walks,
-// and ranks within a 64-token tile with ballots, so all orders are exact and
-// ties are broken by index, deterministically.
+// Stage I narrows a bucket {k : (k & pmask) == prefix} that contains the K1-th
+// smallest key with 8-bit digit passes over the highest still-undecided bits
+// in which some key differs (bytes no key varies in cost nothing).  Each pass
+// is a histogram (ballot "same digit" masks, one LDS atomic per distinct digit
+// per tile) and a DPP scan that picks the digit holding the K1-th key.  It
+// stops when
+//   - the bucket holds a single key value T: keys < T are kept, then the first
+//     keys == T in token order (ordered ballot counts), or
+//   - (images of at most 4096 tokens) the bucket holds at most 128 keys: each
+//     bucket member counts the members smaller than itself in (key, index)
+//     order, exactly, and is kept if that rank is below the remaining budget.
+// Stage II (images of at most 4096 tokens): one bucketing pass, 256 buckets of
+// equal width over the [min, max] of X^rem's keys, places X^rem in bucket
+// order; every token then counts the members of its own bucket smaller in
+// (key, index) order, so its rank in the sorted X^rem is exact.  If a bucket
+// exceeds 128 tokens, the range is not finite, (or
+// for larger images) Stage II falls back to a 4-pass stable LSD radix sort of
+// the 16-bit indices of X^rem (ordered compaction first, digits looked up by
+// index, per-wavefront scatter offsets), with passes over constant bytes
+// skipped.
 //
-// LDS layout for an image of n tokens (W = threads / 64, nw = 2 ceil(n/64)):
-//   ks    u32[n]      Stage II keys by token index
-//   ki    u32[n]      Stage I keys by token index; after Stage I the same bytes
-//                     hold two u16[n] index buffers for the sort
-//   bimp  u32[nw]     X^imp bitmap
-//   bsel  u32[nw]     X^imp U X^div bitmap
-//   hist  u16[256 W]  per-wavefront digit counts / scatter offsets
-//   scan  u32[W + 4]  workgroup scan scratch and broadcast slots
+// Every wavefront owns a contiguous, 64-aligned range of tokens for the
+// ordered steps (tie marking, compaction, output), so all results are exact
+// and deterministic.
 #include "tr_internal.h"
+#include "tr_wave.h"
 
 namespace tr {
 namespace {
 
+constexpr int kThreads = 1024;
+constexpr int kW = kThreads / kWave;
+constexpr int kSmallMaxN = 4096;
+constexpr uint32_t kCountLimit = 128;
+
+// ---- LDS layout (same arithmetic on host and device) -----------------------
+struct LdsLayout {
+    size_t ks, ki, list, bimp, bsel, hsh, cur, hist, slots, misc, total;
+};
+
+__host__ __device__ inline size_t align_up(size_t v, size_t a) { return (v + a - 1) & ~(a - 1); }
+
+//   ks    u32[n]        Stage II keys by token index
+//   ki    u32[n]        Stage I keys; after Stage I two u16[n] index buffers
+//   list  u64[n]        (key << 16 | index) of bucket members (small images)
+//   bimp  u32[nw]       X^imp bitmap (nw = 2 ceil(n / 64))
+//   bsel  u32[nw]       X^imp U X^div bitmap
+//   hsh   u32[2][256]   digit histograms (double buffered), 16-byte aligned
+//   cur   u32[256]      bucket cursors (small images)
+//   hist  u16[256][W]   per-wavefront digit counts / offsets of the LSD sort
+//   slots u32[8][W]     per-wavefront partial counts, one row per use
+//   misc  u32[16]       broadcast slots and counters
+__host__ __device__ inline LdsLayout lds_layout(int n, bool small)
+{
+    LdsLayout L;
+    const size_t nw = 2 * (((size_t)n + 63) / 64);
+    size_t o = 0;
+    L.ks = o;
+    o += 4 * (size_t)n;
+    L.ki = o;
+    o += 4 * (size_t)n;
+    o = align_up(o, 8);
+    L.list = o;
+    if (small) o += 8 * (size_t)n;
+    L.bimp = o;
+    o += 4 * nw;
+    L.bsel = o;
+    o += 4 * nw;
+    o = align_up(o, 16);
+    L.hsh = o;
+    o += 4 * 512;
+    L.cur = o;
+    if (small) o += 4 * 256;
+    L.hist = o;
+    o += 2 * 256 * kW;
+    L.slots = o;
+    o += 4 * 8 * kW;
+    L.misc = o;
+    o += 4 * 16;
+    L.total = o;
+    return L;
+}
+
+// ---- helpers -------------------------------------------------------------------
 // IEEE order -> unsigned order; -0 and +0 map to the same key.
 __device__ __forceinline__ uint32_t order_key(float f)
 {
@@ -35,10 +97,7 @@ __device__ __forceinline__ uint32_t order_key(float f)
     return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-__device__ __forceinline__ uint64_t lanes_below(int lane)
-{
-    return (1ull << lane) - 1ull;
-}
+__device__ __forceinline__ uint64_t lanes_below(int lane) { return (1ull << lane) - 1ull; }
 
 // Mask of active lanes whose 8-bit digit equals this lane's digit.
 __device__ __forceinline__ uint64_t same_digit(uint32_t digit, bool active)
@@ -53,46 +112,12 @@ __device__ __forceinline__ uint64_t same_digit(uint32_t digit, bool active)
     return m;
 }
 
-// Exclusive prefix over the wavefronts of a per-wavefront count (every lane of
-// a wavefront passes the same value).  Returns the count of earlier waves.
-template <int W>
-__device__ __forceinline__ uint32_t wave_prefix(uint32_t count, uint32_t* scan)
+__device__ __forceinline__ bool is_leader(uint64_t m, int lane)
 {
-    const int lane = threadIdx.x & (kWave - 1);
-    const int w = threadIdx.x / kWave;
-    if (lane == 0) scan[w] = count;
-    __syncthreads();
-    uint32_t base = 0;
-    for (int i = 0; i < w; ++i) base += scan[i];
-    __syncthreads();
-    return base;
+    return m && (int)(__ffsll((long long)m) - 1) == lane;
 }
 
-// Exclusive prefix of one value per thread over the whole workgroup.
-template <int THREADS>
-__device__ __forceinline__ uint32_t block_prefix(uint32_t v, uint32_t* scan)
-{
-    constexpr int W = THREADS / kWave;
-    const int lane = threadIdx.x & (kWave - 1);
-    const int w = threadIdx.x / kWave;
-    uint32_t x = v;
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-        const uint32_t y = __shfl_up(x, o, kWave);
-        if (lane >= o) x += y;
-    }
-    if (lane == kWave - 1) scan[w] = x;
-    __syncthreads();
-    uint32_t base = 0;
-    for (int i = 0; i < W && i < w; ++i) base += scan[i];
-    __syncthreads();
-    return base + x - v;
-}
-
-__device__ __forceinline__ bool bit_of(const uint32_t* bm, int i)
-{
-    return (bm[i >> 5] >> (i & 31)) & 1u;
-}
+__device__ __forceinline__ bool bit_of(const uint32_t* bm, int i) { return (bm[i >> 5] >> (i & 31)) & 1u; }
 
 // A wavefront writes the 64-bit ballot of tile `base` into two bitmap words.
 __device__ __forceinline__ void put_tile_bits(uint32_t* bm, int base, uint64_t bits, int lane)
@@ -101,14 +126,33 @@ __device__ __forceinline__ void put_tile_bits(uint32_t* bm, int base, uint64_t b
     if (lane == 32) bm[(base >> 5) + 1] = (uint32_t)(bits >> 32);
 }
 
-template <int THREADS>
-__global__ __launch_bounds__(THREADS) void select_kernel(SelectArgs a)
+// Contiguous 64-aligned token range of wavefront w.
+__device__ __forceinline__ void wave_range(int n, int w, int& beg, int& end)
 {
-    constexpr int W = THREADS / kWave;
-    extern __shared__ __align__(16) unsigned char smem[];
+    const int seg = (((n + kW - 1) / kW) + 63) & ~63;
+    beg = w * seg < n ? w * seg : n;
+    end = beg + seg < n ? beg + seg : n;
+}
+
+// Exclusive prefix over wavefronts of a per-wavefront count (each row of
+// slots is used once per kernel).
+__device__ __forceinline__ uint32_t wave_prefix(uint32_t count, uint32_t* row)
+{
     const int lane = threadIdx.x & (kWave - 1);
     const int w = threadIdx.x / kWave;
+    if (lane == 0) row[w] = count;
+    __syncthreads();
+    uint32_t base = 0;
+    for (int i = 0; i < w; ++i) base += row[i];
+    return base;
+}
 
+struct Img {
+    int row_off, n, k1, k2, t, out_off;
+};
+
+__device__ __forceinline__ Img image_of(const SelectArgs& a)
+{
     ImageDesc d;
     if (a.uniform) {
         d = a.desc[0];
@@ -118,193 +162,411 @@ __global__ __launch_bounds__(THREADS) void select_kernel(SelectArgs a)
     } else {
         d = a.desc[blockIdx.x];
     }
-    const int N = d.n, K1 = d.k1, K2 = d.k2, t = d.t;
-    const int nw = 2 * ((N + 63) / 64);
+    return Img{d.row_off, d.n, d.k1, d.k2, d.t, d.out_off};
+}
 
-    uint32_t* ks = reinterpret_cast<uint32_t*>(smem);
-    uint32_t* ki = ks + N;
-    uint16_t* idx_a = reinterpret_cast<uint16_t*>(ki);
-    uint16_t* idx_b = idx_a + N;
-    uint32_t* bimp = ki + N;
-    uint32_t* bsel = bimp + nw;
-    uint16_t* hist = reinterpret_cast<uint16_t*>(bsel + nw);
-    uint32_t* scan = reinterpret_cast<uint32_t*>(hist + 256 * W);
-
-    // Wavefront ranges over the n tokens.
-    const int segN = (((N + W - 1) / W) + 63) & ~63;
-    const int begN = w * segN < N ? w * segN : N;
-    const int endN = begN + segN < N ? begN + segN : N;
-
-    // ---- load keys ---------------------------------------------------------
-    for (int i = threadIdx.x; i < N; i += THREADS) {
-        ks[i] = order_key(a.key_s[d.row_off + i]);
-        ki[i] = order_key(a.key_imp[d.row_off + i]);
+// ---- phases ------------------------------------------------------------------
+// Load the image's keys (all global loads of a batch issued before the LDS
+// stores), zero `nzero` words at `zero`, and return the bits in which some key
+// differs from token 0's key.
+__device__ void load_keys(const SelectArgs& a, const Img& d, uint32_t* ki, uint32_t* ks,
+                          uint32_t* zero, int nzero, uint32_t* slots, uint32_t& k0i,
+                          uint32_t& VI, uint32_t& VS)
+{
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
+    const int N = d.n;
+    k0i = order_key(a.key_imp[d.row_off]);
+    const uint32_t k0s = order_key(a.key_s[d.row_off]);
+    uint32_t vi = 0, vs = 0;
+    for (int i0 = tid; i0 < N; i0 += 4 * kThreads) {
+        float fi[4], fs[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int i = i0 + u * kThreads;
+            if (i < N) {
+                fi[u] = a.key_imp[d.row_off + i];
+                fs[u] = a.key_s[d.row_off + i];
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int i = i0 + u * kThreads;
+            if (i < N) {
+                const uint32_t qi = order_key(fi[u]), qs = order_key(fs[u]);
+                ki[i] = qi;
+                ks[i] = qs;
+                vi |= qi ^ k0i;
+                vs |= qs ^ k0s;
+            }
+        }
+    }
+    for (int i = tid; i < nzero; i += kThreads) zero[i] = 0;
+    vi = wave_or_u32(vi);
+    vs = wave_or_u32(vs);
+    if (lane == 0) {
+        slots[w] = vi;
+        slots[kW + w] = vs;
     }
     __syncthreads();
-
-    // ---- Stage I: radix select of the K1-th smallest key --------------------
-    uint32_t T = 0;
-    uint32_t need = 0;   // keys equal to T that are taken, in index order
-    if (K1 > 0 && K1 < N) {
-        uint32_t prefix = 0, pmask = 0;
-        need = (uint32_t)K1;
-        for (int shift = 24; shift >= 0; shift -= 8) {
-            for (int i = threadIdx.x; i < 256 * W; i += THREADS) hist[i] = 0;
-            __syncthreads();
-            for (int base = begN; base < endN; base += kWave) {
-                const int i = base + lane;
-                bool act = i < endN;
-                const uint32_t key = act ? ki[i] : 0u;
-                act = act && ((key & pmask) == prefix);
-                const uint32_t dg = (key >> shift) & 255u;
-                const uint64_t m = same_digit(dg, act);
-                if (act && (int)(__ffsll((long long)m) - 1) == lane)
-                    hist[dg * W + w] = (uint16_t)(hist[dg * W + w] + __popcll(m));
-            }
-            __syncthreads();
-            if (w == 0) {
-                uint32_t cnt[4], sum = 0;
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    uint32_t c = 0;
-                    for (int ww = 0; ww < W; ++ww) c += hist[(lane * 4 + q) * W + ww];
-                    cnt[q] = c;
-                    sum += c;
-                }
-                uint32_t x = sum;
-#pragma unroll
-                for (int o = 1; o < kWave; o <<= 1) {
-                    const uint32_t y = __shfl_up(x, o, kWave);
-                    if (lane >= o) x += y;
-                }
-                uint32_t run = x - sum;
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    if (run < need && need <= run + cnt[q]) {
-                        scan[W] = (uint32_t)(lane * 4 + q);
-                        scan[W + 1] = need - run;
-                    }
-                    run += cnt[q];
-                }
-            }
-            __syncthreads();
-            const uint32_t dsel = scan[W];
-            need = scan[W + 1];
-            prefix |= dsel << shift;
-            pmask |= 255u << shift;
-            __syncthreads();
-        }
-        T = prefix;
+    VI = 0;
+    VS = 0;
+    for (int i = 0; i < kW; ++i) {
+        VI |= slots[i];
+        VS |= slots[kW + i];
     }
+}
 
-    // ---- Stage I: mark X^imp (keys < T, then the first `need` keys == T) ----
-    if (K1 == 0 || K1 == N) {
-        const uint32_t fill = K1 ? 0xffffffffu : 0u;
-        for (int i = threadIdx.x; i < nw; i += THREADS) bimp[i] = fill;
-    } else {
-        uint32_t eq = 0;
-        for (int base = begN; base < endN; base += kWave) {
-            const int i = base + lane;
-            eq += __popcll(__ballot(i < endN && ki[i] == T));
+// Stage I digit passes (see the file comment).  On return the bucket
+// {k : (k & pmask) == prefix} holds m keys and the K1-th smallest key overall
+// is its need-th smallest; resolved means the bucket is a single key value.
+__device__ void stage1_narrow(const uint32_t* ki, int N, uint32_t VI, uint32_t* hsh, uint32_t* misc,
+                              uint32_t limit, uint32_t& prefix, uint32_t& pmask, uint32_t& need,
+                              uint32_t& m, bool& resolved)
+{
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
+    int beg, end;
+    wave_range(N, w, beg, end);
+    resolved = false;
+    for (int p = 0;; ++p) {
+        const uint32_t vrem = VI & ~pmask;
+        if (vrem == 0) {
+            resolved = true;
+            return;
         }
-        uint32_t rank = wave_prefix<W>(eq, scan);
-        for (int base = begN; base < endN; base += kWave) {
+        if (m <= limit) return;
+        const int hb = 31 - __clz((int)vrem);
+        const int lo = hb >= 7 ? hb - 7 : 0;
+        const uint32_t win = (hb == 31 ? 0xffffffffu : ((2u << hb) - 1u)) & ~((1u << lo) - 1u);
+        uint32_t* H = hsh + (p & 1) * 256;
+        if (tid < 256) hsh[((p + 1) & 1) * 256 + tid] = 0;   // the next pass's histogram
+        for (int base = beg; base < end; base += kWave) {
             const int i = base + lane;
-            const bool act = i < endN;
-            const uint32_t key = act ? ki[i] : 0xffffffffu;
-            const bool is_eq = act && key == T;
-            const uint64_t be = __ballot(is_eq);
-            const uint32_t r = rank + (uint32_t)__popcll(be & lanes_below(lane));
-            const bool take = act && (key < T || (is_eq && r < need));
-            put_tile_bits(bimp, base, __ballot(take), lane);
-            rank += (uint32_t)__popcll(be);
-        }
-    }
-    __syncthreads();   // ki is dead from here on; its bytes become idx_a / idx_b
-
-    // ---- Stage II: X^rem in index order, stable radix sort by s, stride -----
-    for (int i = threadIdx.x; i < nw; i += THREADS) bsel[i] = bimp[i];
-    if (K2 > 0) {
-        uint32_t rc = 0;
-        for (int base = begN; base < endN; base += kWave) {
-            const int i = base + lane;
-            rc += __popcll(__ballot(i < endN && !bit_of(bimp, i)));
-        }
-        uint32_t pos = wave_prefix<W>(rc, scan);
-        for (int base = begN; base < endN; base += kWave) {
-            const int i = base + lane;
-            const bool keep = i < endN && !bit_of(bimp, i);
-            const uint64_t bk = __ballot(keep);
-            if (keep) idx_a[pos + __popcll(bk & lanes_below(lane))] = (uint16_t)i;
-            pos += (uint32_t)__popcll(bk);
+            bool act = i < end;
+            const uint32_t key = act ? ki[i] : 0u;
+            act = act && ((key & pmask) == prefix);
+            const uint32_t dg = (key >> lo) & 255u;
+            const uint64_t mm = same_digit(dg, act);
+            if (act && is_leader(mm, lane)) atomicAdd(&H[dg], (uint32_t)__popcll(mm));
         }
         __syncthreads();
-
-        const int R = N - K1;
-        const int segR = (((R + W - 1) / W) + 63) & ~63;
-        const int begR = w * segR < R ? w * segR : R;
-        const int endR = begR + segR < R ? begR + segR : R;
-        uint16_t* src = idx_a;
-        uint16_t* dst = idx_b;
-        for (int shift = 0; shift < 32; shift += 8) {
-            for (int i = threadIdx.x; i < 256 * W; i += THREADS) hist[i] = 0;
-            __syncthreads();
-            for (int base = begR; base < endR; base += kWave) {
-                const int i = base + lane;
-                const bool act = i < endR;
-                const uint32_t id = act ? src[i] : 0u;
-                const uint32_t dg = act ? (ks[id] >> shift) & 255u : 0u;
-                const uint64_t m = same_digit(dg, act);
-                if (act && (int)(__ffsll((long long)m) - 1) == lane)
-                    hist[dg * W + w] = (uint16_t)(hist[dg * W + w] + __popcll(m));
+        if (w == 0) {
+            const uint4 c4 = *reinterpret_cast<const uint4*>(H + lane * 4);
+            const uint32_t c[4] = {c4.x, c4.y, c4.z, c4.w};
+            const uint32_t sum = c[0] + c[1] + c[2] + c[3];
+            uint32_t run = wave_scan_add(sum) - sum;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                if (run < need && need <= run + c[q]) {
+                    misc[0] = (uint32_t)(lane * 4 + q);
+                    misc[1] = need - run;
+                    misc[2] = c[q];
+                }
+                run += c[q];
             }
-            __syncthreads();
-            {   // exclusive scan of hist in (digit, wavefront) order, 4 entries per thread
-                const int e = threadIdx.x * 4;
-                const uint32_t h0 = hist[e], h1 = hist[e + 1], h2 = hist[e + 2], h3 = hist[e + 3];
-                const uint32_t b0 = block_prefix<THREADS>(h0 + h1 + h2 + h3, scan);
-                hist[e] = (uint16_t)b0;
-                hist[e + 1] = (uint16_t)(b0 + h0);
-                hist[e + 2] = (uint16_t)(b0 + h0 + h1);
-                hist[e + 3] = (uint16_t)(b0 + h0 + h1 + h2);
-            }
-            __syncthreads();
-            for (int base = begR; base < endR; base += kWave) {
-                const int i = base + lane;
-                const bool act = i < endR;
-                const uint32_t id = act ? src[i] : 0u;
-                const uint32_t dg = act ? (ks[id] >> shift) & 255u : 0u;
-                const uint64_t m = same_digit(dg, act);
-                const uint32_t off = act ? hist[dg * W + w] : 0u;
-                if (act) dst[off + __popcll(m & lanes_below(lane))] = (uint16_t)id;
-                if (act && (int)(__ffsll((long long)m) - 1) == lane)
-                    hist[dg * W + w] = (uint16_t)(off + __popcll(m));
-            }
-            __syncthreads();
-            uint16_t* tmp = src;
-            src = dst;
-            dst = tmp;
         }
-        for (int j = threadIdx.x; j < K2; j += THREADS) {
-            const int id = src[j * t];
-            atomicOr(&bsel[id >> 5], 1u << (id & 31));
+        __syncthreads();
+        prefix |= misc[0] << lo;
+        need = misc[1];
+        m = misc[2];
+        pmask |= win;
+    }
+}
+
+// Stage I marking with a resolved threshold key T: keys < T, then the first
+// `need` keys == T in token order.
+__device__ void stage1_mark_resolved(const uint32_t* ki, int N, uint32_t T, uint32_t need,
+                                     uint32_t* bimp, uint32_t* bsel, uint32_t* row)
+{
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
+    int beg, end;
+    wave_range(N, w, beg, end);
+    uint32_t eq = 0;
+    for (int base = beg; base < end; base += kWave) {
+        const int i = base + lane;
+        eq += __popcll(__ballot(i < end && ki[i] == T));
+    }
+    uint32_t rank = wave_prefix(eq, row);
+    for (int base = beg; base < end; base += kWave) {
+        const int i = base + lane;
+        const bool act = i < end;
+        const uint32_t key = act ? ki[i] : 0xffffffffu;
+        const bool is_eq = act && key == T;
+        const uint64_t be = __ballot(is_eq);
+        const uint32_t r = rank + (uint32_t)__popcll(be & lanes_below(lane));
+        const bool take = act && (key < T || (is_eq && r < need));
+        const uint64_t bt = __ballot(take);
+        put_tile_bits(bimp, base, bt, lane);
+        put_tile_bits(bsel, base, bt, lane);
+        rank += (uint32_t)__popcll(be);
+    }
+}
+
+// Stage I marking by exact counting inside a bucket of at most kCountLimit
+// keys: keys below the bucket are kept, and a member is kept when fewer than
+// `need` members precede it in (key, index) order.  misc[8] must be 0.
+__device__ void stage1_mark_counted(const uint32_t* ki, int N, uint32_t prefix, uint32_t pmask,
+                                    uint32_t need, uint64_t* list, uint32_t* misc, uint32_t* bimp,
+                                    uint32_t* bsel)
+{
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
+    int beg, end;
+    wave_range(N, w, beg, end);
+    for (int base = beg; base < end; base += kWave) {
+        const int i = base + lane;
+        const bool act = i < end;
+        const uint32_t key = act ? ki[i] : 0u;
+        const bool member = act && (key & pmask) == prefix;
+        const uint64_t bm = __ballot(member);
+        if (bm) {
+            const int leader = (int)__ffsll((long long)bm) - 1;
+            uint32_t b0 = 0;
+            if (lane == leader) b0 = atomicAdd(&misc[8], (uint32_t)__popcll(bm));
+            b0 = (uint32_t)__builtin_amdgcn_readlane((int)b0, leader);
+            if (member) list[b0 + __popcll(bm & lanes_below(lane))] = ((uint64_t)key << 16) | (uint32_t)i;
         }
     }
     __syncthreads();
-
-    // ---- X* in ascending token index ---------------------------------------
-    uint32_t oc = 0;
-    for (int base = begN; base < endN; base += kWave) {
+    const uint32_t m = misc[8];
+    for (int base = beg; base < end; base += kWave) {
         const int i = base + lane;
-        oc += __popcll(__ballot(i < endN && bit_of(bsel, i)));
+        const bool act = i < end;
+        const uint32_t key = act ? ki[i] : 0u;
+        const bool member = act && (key & pmask) == prefix;
+        const bool below = act && (key & pmask) < prefix;
+        uint32_t r = 0;
+        if (member) {
+            const uint64_t mine = ((uint64_t)key << 16) | (uint32_t)i;
+            for (uint32_t j = 0; j < m; ++j) r += list[j] < mine ? 1u : 0u;
+        }
+        const uint64_t bt = __ballot(below || (member && r < need));
+        put_tile_bits(bimp, base, bt, lane);
+        put_tile_bits(bsel, base, bt, lane);
     }
-    uint32_t opos = wave_prefix<W>(oc, scan);
-    for (int base = begN; base < endN; base += kWave) {
+}
+
+// Inverse of order_key.
+__device__ __forceinline__ float key_value(uint32_t k)
+{
+    return __uint_as_float((k & 0x80000000u) ? (k ^ 0x80000000u) : ~k);
+}
+
+// Stage II by one bucketing pass and exact counting inside buckets.  Bucket
+// d of a remaining token is floor((s - s_min) * 256 / (s_max - s_min)) over
+// the remainder's key range, a non-decreasing function of s in fp32 (every
+// step rounds monotonically), so bucket order agrees with key order and the
+// exact (key, index) count inside a bucket gives the exact rank.  H (256
+// words) must be zero.  Returns false, having changed nothing but H, cur,
+// list and misc[3..5], when a bucket holds more than kCountLimit tokens or
+// the range is not finite.
+__device__ bool stage2_bucket(const uint32_t* ks, const uint32_t* bimp, uint32_t* bsel, int N,
+                              int K2, int t, uint32_t* H, uint32_t* cur, uint64_t* list,
+                              uint32_t* misc, uint32_t* row_lo, uint32_t* row_hi, uint32_t* row)
+{
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
+    int beg, end;
+    wave_range(N, w, beg, end);
+    const uint32_t span = (uint32_t)K2 * (uint32_t)t;
+
+    // key range of X^rem (max of the complement gives the minimum)
+    uint32_t nlo = 0, hi = 0;
+    for (int base = beg; base < end; base += kWave) {
         const int i = base + lane;
-        const bool kept = i < endN && bit_of(bsel, i);
+        if (i < end && !bit_of(bimp, i)) {
+            nlo = max(nlo, ~ks[i]);
+            hi = max(hi, ks[i]);
+        }
+    }
+    nlo = wave_max_u32(nlo);
+    hi = wave_max_u32(hi);
+    if (lane == 0) {
+        row_lo[w] = nlo;
+        row_hi[w] = hi;
+    }
+    __syncthreads();
+    uint32_t kmin = 0, kmax = 0;
+    for (int i = 0; i < kW; ++i) {
+        kmin = max(kmin, row_lo[i]);
+        kmax = max(kmax, row_hi[i]);
+    }
+    kmin = ~kmin;
+
+    if (kmin == kmax) {
+        // Every remaining key is equal: the stable order is the token order of X^rem.
+        uint32_t rc = 0;
+        for (int base = beg; base < end; base += kWave) {
+            const int i = base + lane;
+            rc += __popcll(__ballot(i < end && !bit_of(bimp, i)));
+        }
+        uint32_t r0 = wave_prefix(rc, row);
+        for (int base = beg; base < end; base += kWave) {
+            const int i = base + lane;
+            const bool rem = i < end && !bit_of(bimp, i);
+            const uint64_t br = __ballot(rem);
+            const uint32_t r = r0 + (uint32_t)__popcll(br & lanes_below(lane));
+            const uint64_t bp = __ballot(rem && r % (uint32_t)t == 0 && r < span);
+            if (lane == 0) bsel[base >> 5] = bimp[base >> 5] | (uint32_t)bp;
+            if (lane == 32) bsel[(base >> 5) + 1] = bimp[(base >> 5) + 1] | (uint32_t)(bp >> 32);
+            r0 += (uint32_t)__popcll(br);
+        }
+        return true;
+    }
+    const float fmin = key_value(kmin);
+    const float width = key_value(kmax) - fmin;
+    if (!(width > 0.f) || !(width < 3.0e38f)) return false;   // not finite: sort instead
+    const float scale = 256.f / width;
+
+    for (int base = beg; base < end; base += kWave) {
+        const int i = base + lane;
+        const bool rem = i < end && !bit_of(bimp, i);
+        uint32_t dg = 0;
+        if (rem) dg = (uint32_t)min(255, (int)((key_value(ks[i]) - fmin) * scale));
+        const uint64_t mm = same_digit(dg, rem);
+        if (rem && is_leader(mm, lane)) atomicAdd(&H[dg], (uint32_t)__popcll(mm));
+    }
+    __syncthreads();
+    if (w == 0) {
+        const uint4 c4 = *reinterpret_cast<const uint4*>(H + lane * 4);
+        const uint32_t sum = c4.x + c4.y + c4.z + c4.w;
+        const uint32_t start = wave_scan_add(sum) - sum;
+        *reinterpret_cast<uint4*>(cur + lane * 4) =
+            make_uint4(start, start + c4.x, start + c4.x + c4.y, start + c4.x + c4.y + c4.z);
+        const uint32_t mx = wave_max_u32(max(max(c4.x, c4.y), max(c4.z, c4.w)));
+        if (lane == 0) misc[3] = mx;
+    }
+    __syncthreads();
+    if (misc[3] > kCountLimit) return false;
+    for (int base = beg; base < end; base += kWave) {
+        const int i = base + lane;
+        const bool rem = i < end && !bit_of(bimp, i);
+        const uint32_t key = rem ? ks[i] : 0u;
+        uint32_t dg = 0;
+        if (rem) dg = (uint32_t)min(255, (int)((key_value(key) - fmin) * scale));
+        const uint64_t mm = same_digit(dg, rem);
+        const int leader = mm ? (int)__ffsll((long long)mm) - 1 : lane;
+        uint32_t b0 = 0;
+        if (rem && leader == lane) b0 = atomicAdd(&cur[dg], (uint32_t)__popcll(mm));
+        b0 = (uint32_t)__shfl((int)b0, leader, kWave);
+        if (rem) list[b0 + __popcll(mm & lanes_below(lane))] = ((uint64_t)key << 16) | (uint32_t)i;
+    }
+    __syncthreads();
+    for (int base = beg; base < end; base += kWave) {
+        const int i = base + lane;
+        const bool rem = i < end && !bit_of(bimp, i);
+        bool picked = false;
+        if (rem) {
+            const uint32_t key = ks[i];
+            const uint32_t dg = (uint32_t)min(255, (int)((key_value(key) - fmin) * scale));
+            const uint32_t stop = cur[dg];
+            const uint32_t start = stop - H[dg];
+            const uint64_t mine = ((uint64_t)key << 16) | (uint32_t)i;
+            uint32_t r = start;
+            for (uint32_t j = start; j < stop; ++j) r += list[j] < mine ? 1u : 0u;
+            picked = r % (uint32_t)t == 0 && r < span;
+        }
+        const uint64_t bp = __ballot(picked);
+        if (lane == 0) bsel[base >> 5] = bimp[base >> 5] | (uint32_t)bp;
+        if (lane == 32) bsel[(base >> 5) + 1] = bimp[(base >> 5) + 1] | (uint32_t)(bp >> 32);
+    }
+    return true;
+}
+
+// Stage II by ordered compaction and a stable LSD radix sort of 16-bit
+// indices; sets the X^div bits in bsel.  idx_a / idx_b hold n u16 each.
+__device__ void stage2_radix(const uint32_t* ks, const uint32_t* bimp, uint32_t* bsel, int N, int K1,
+                             int K2, int t, uint32_t VS, uint16_t* idx_a, uint16_t* idx_b,
+                             uint16_t* hist, uint32_t* row_c, uint32_t* row_s)
+{
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
+    int beg, end;
+    wave_range(N, w, beg, end);
+    uint32_t rc = 0;
+    for (int base = beg; base < end; base += kWave) {
+        const int i = base + lane;
+        rc += __popcll(__ballot(i < end && !bit_of(bimp, i)));
+    }
+    uint32_t pos = wave_prefix(rc, row_c);
+    for (int base = beg; base < end; base += kWave) {
+        const int i = base + lane;
+        const bool keep = i < end && !bit_of(bimp, i);
+        const uint64_t bk = __ballot(keep);
+        if (keep) idx_a[pos + __popcll(bk & lanes_below(lane))] = (uint16_t)i;
+        pos += (uint32_t)__popcll(bk);
+    }
+    const int R = N - K1;
+    int begR, endR;
+    wave_range(R, w, begR, endR);
+    uint16_t* src = idx_a;
+    uint16_t* dst = idx_b;
+    for (int shift = 0; shift < 32; shift += 8) {
+        if (((VS >> shift) & 255u) == 0) continue;   // every key has the same byte here
+        uint32_t* h32 = reinterpret_cast<uint32_t*>(hist);
+        for (int i = tid; i < 128 * kW; i += kThreads) h32[i] = 0;
+        __syncthreads();
+        for (int base = begR; base < endR; base += kWave) {
+            const int i = base + lane;
+            const bool act = i < endR;
+            const uint32_t id = act ? src[i] : 0u;
+            const uint32_t dg = act ? (ks[id] >> shift) & 255u : 0u;
+            const uint64_t m = same_digit(dg, act);
+            if (act && is_leader(m, lane)) hist[dg * kW + w] = (uint16_t)(hist[dg * kW + w] + __popcll(m));
+        }
+        __syncthreads();
+        {   // exclusive scan of hist in (digit, wavefront) order, 4 entries per thread
+            const int e = tid * 4;
+            const uint2 hv = *reinterpret_cast<const uint2*>(hist + e);
+            const uint32_t h0 = hv.x & 0xffffu, h1 = hv.x >> 16, h2 = hv.y & 0xffffu, h3 = hv.y >> 16;
+            const uint32_t v = h0 + h1 + h2 + h3;
+            const uint32_t inc = wave_scan_add(v);
+            if (lane == kWave - 1) row_s[w] = inc;
+            __syncthreads();
+            uint32_t b0 = inc - v;
+            for (int i = 0; i < w; ++i) b0 += row_s[i];
+            const uint32_t o1 = b0 + h0, o2 = o1 + h1, o3 = o2 + h2;
+            *reinterpret_cast<uint2*>(hist + e) = make_uint2(b0 | (o1 << 16), o2 | (o3 << 16));
+        }
+        __syncthreads();
+        for (int base = begR; base < endR; base += kWave) {
+            const int i = base + lane;
+            const bool act = i < endR;
+            const uint32_t id = act ? src[i] : 0u;
+            const uint32_t dg = act ? (ks[id] >> shift) & 255u : 0u;
+            const uint64_t m = same_digit(dg, act);
+            const uint32_t off = act ? hist[dg * kW + w] : 0u;
+            if (act) dst[off + __popcll(m & lanes_below(lane))] = (uint16_t)id;
+            if (act && is_leader(m, lane)) hist[dg * kW + w] = (uint16_t)(off + __popcll(m));
+        }
+        __syncthreads();
+        uint16_t* tmp = src;
+        src = dst;
+        dst = tmp;
+    }
+    __syncthreads();   // the compaction (or the last pass) is visible to every picker
+    for (int j = tid; j < K2; j += kThreads) {
+        const int id = src[j * t];
+        atomicOr(&bsel[id >> 5], 1u << (id & 31));
+    }
+}
+
+// X* in ascending token index: out_idx (image-local), out_src, out_rows.
+__device__ void emit(const SelectArgs& a, const Img& d, const uint32_t* bimp, const uint32_t* bsel,
+                     uint32_t* row)
+{
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
+    int beg, end;
+    wave_range(d.n, w, beg, end);
+    uint32_t oc = 0;
+    for (int base = beg; base < end; base += kWave) {
+        const int i = base + lane;
+        oc += __popcll(__ballot(i < end && bit_of(bsel, i)));
+    }
+    uint32_t opos = wave_prefix(oc, row);
+    const int K = d.k1 + d.k2;
+    for (int base = beg; base < end; base += kWave) {
+        const int i = base + lane;
+        const bool kept = i < end && bit_of(bsel, i);
         const uint64_t bk = __ballot(kept);
         const int slot = (int)opos + __popcll(bk & lanes_below(lane));
-        if (kept && slot < K1 + K2) {   // never more than K writes, whatever the keys
+        if (kept && slot < K) {   // never more than K writes, whatever the keys
             const int o = d.out_off + slot;
             a.out_idx[o] = i;
             if (a.out_src) a.out_src[o] = bit_of(bimp, i) ? 0 : 1;
@@ -314,38 +576,97 @@ __global__ __launch_bounds__(THREADS) void select_kernel(SelectArgs a)
     }
 }
 
+template <bool SMALL>
+__global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a)
+{
+    extern __shared__ __align__(16) unsigned char smem[];
+    const Img d = image_of(a);
+    const int N = d.n, K1 = d.k1, K2 = d.k2;
+    const LdsLayout L = lds_layout(N, SMALL);
+    uint32_t* ks = reinterpret_cast<uint32_t*>(smem + L.ks);
+    uint32_t* ki = reinterpret_cast<uint32_t*>(smem + L.ki);
+    uint64_t* list = reinterpret_cast<uint64_t*>(smem + L.list);
+    uint32_t* bimp = reinterpret_cast<uint32_t*>(smem + L.bimp);
+    uint32_t* bsel = reinterpret_cast<uint32_t*>(smem + L.bsel);
+    uint32_t* hsh = reinterpret_cast<uint32_t*>(smem + L.hsh);
+    uint32_t* cur = reinterpret_cast<uint32_t*>(smem + L.cur);
+    uint16_t* hist = reinterpret_cast<uint16_t*>(smem + L.hist);
+    uint32_t* slots = reinterpret_cast<uint32_t*>(smem + L.slots);
+    uint32_t* misc = reinterpret_cast<uint32_t*>(smem + L.misc);
+    const int nw = 2 * ((N + 63) / 64);
+
+    // hsh (512 words) and misc (16 words) start at zero
+    uint32_t k0i, VI, VS;
+    if (threadIdx.x < 16) misc[threadIdx.x] = 0;
+    load_keys(a, d, ki, ks, hsh, 512, slots, k0i, VI, VS);
+
+    // ---- Stage I ---------------------------------------------------------------
+    if (K1 == 0 || K1 == N) {
+        const uint32_t fill = K1 ? 0xffffffffu : 0u;
+        for (int i = threadIdx.x; i < nw; i += kThreads) {
+            bimp[i] = fill;
+            bsel[i] = fill;
+        }
+    } else {
+        uint32_t prefix = k0i & ~VI, pmask = ~VI, need = (uint32_t)K1, m = (uint32_t)N;
+        bool resolved;
+        stage1_narrow(ki, N, VI, hsh, misc, SMALL ? kCountLimit : 0u, prefix, pmask, need, m, resolved);
+        if (resolved) stage1_mark_resolved(ki, N, prefix, need, bimp, bsel, slots + 2 * kW);
+        else stage1_mark_counted(ki, N, prefix, pmask, need, list, misc, bimp, bsel);
+    }
+    __syncthreads();   // the Stage I histograms are read no more; ki is dead
+    // hsh's first 256 words become the Stage II histogram
+    if (threadIdx.x < 256) hsh[threadIdx.x] = 0;
+    __syncthreads();
+
+    // ---- Stage II --------------------------------------------------------------
+    if (K2 > 0) {
+        bool done = false;
+        if (SMALL)
+            done = stage2_bucket(ks, bimp, bsel, N, K2, d.t, hsh, cur, list, misc, slots + 3 * kW,
+                                 slots + 7 * kW, slots + 1 * kW);
+        if (!done) {
+            uint16_t* idx_a = reinterpret_cast<uint16_t*>(ki);
+            stage2_radix(ks, bimp, bsel, N, K1, K2, d.t, VS, idx_a, idx_a + N, hist, slots + 4 * kW,
+                         slots + 5 * kW);
+        }
+    }
+    __syncthreads();
+    emit(a, d, bimp, bsel, slots + 6 * kW);
+}
+
 }  // namespace
 
 int select_threads(int nmax)
 {
-    return nmax > 4096 ? 1024 : 256;
+    (void)nmax;
+    return kThreads;
 }
 
 size_t select_lds_bytes(int n, int threads)
 {
-    const size_t W = (size_t)threads / kWave;
-    const size_t nw = 2 * (((size_t)n + 63) / 64);
-    return 8 * (size_t)n + 8 * nw + 512 * W + 4 * (W + 4);
+    (void)threads;
+    return lds_layout(n, n <= kSmallMaxN).total;
 }
 
 hipError_t select_prepare(int lds_limit)
 {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&select_kernel<1024>),
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&select_kernel<false>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, lds_limit);
     if (e != hipSuccess) return e;
-    return hipFuncSetAttribute(reinterpret_cast<const void*>(&select_kernel<256>),
+    return hipFuncSetAttribute(reinterpret_cast<const void*>(&select_kernel<true>),
                                hipFuncAttributeMaxDynamicSharedMemorySize, lds_limit);
 }
 
 hipError_t launch_select(const SelectArgs& a, int nmax, hipStream_t s)
 {
     if (a.nimg <= 0) return hipSuccess;
-    const int threads = select_threads(nmax);
-    const size_t lds = select_lds_bytes(nmax, threads);
-    if (threads == 1024)
-        hipLaunchKernelGGL(select_kernel<1024>, dim3(a.nimg), dim3(1024), lds, s, a);
+    const bool small = nmax <= kSmallMaxN;
+    const size_t lds = lds_layout(nmax, small).total;
+    if (small)
+        hipLaunchKernelGGL(select_kernel<true>, dim3(a.nimg), dim3(kThreads), lds, s, a);
     else
-        hipLaunchKernelGGL(select_kernel<256>, dim3(a.nimg), dim3(256), lds, s, a);
+        hipLaunchKernelGGL(select_kernel<false>, dim3(a.nimg), dim3(kThreads), lds, s, a);
     return hipGetLastError();
 }
 

@@ -176,14 +176,33 @@ def test_select_bit_exact_on_given_keys():
     cases.append(([18432], [1152], 1 / 3))
     cases.append(([65] * 40, [13] * 40, 1 / 3))                       # > 32 images, uniform
     cases.append(([65, 70] * 20, [13, 14] * 20, 1 / 3))               # > 32 images, ragged
-    for ci, (N, K, lam) in enumerate(cases):
-        say("select keys case", ci, "B", len(N), "lam", lam)
+    # key shapes that steer the selection's internal paths: all keys equal,
+    # one outlier that puts every other key in one bucket, narrow clusters
+    shaped = []
+    for n in (100, 576, 3000, 4096, 5000):
+        for shape in ("const", "outlier", "narrow"):
+            shaped.append(([n], [max(1, n // 9)], 1 / 3, shape))
+    cases = [c + ("mixed",) for c in cases] + shaped
+    for ci, (N, K, lam, shape) in enumerate(cases):
+        say("select keys case", ci, "B", len(N), "lam", lam, "shape", shape)
         total = sum(N)
-        # keys drawn from small value sets plant exact ties, and include -0.0/+0.0
-        ki = rng.choice(np.array([0.0, -0.0, 1.5, 2.25, -7.0, 3e-8, 1e30], np.float32), size=total)
-        ki = np.where(rng.random(total) < 0.5, ki, rng.standard_normal(total).astype(np.float32))
-        ks = rng.choice(np.array([-1.0, -0.0, 0.0, 0.5, 0.25, 1.0], np.float32), size=total)
-        ks = np.where(rng.random(total) < 0.5, ks, rng.uniform(-1, 1, total).astype(np.float32))
+        if shape == "mixed":
+            # keys drawn from small value sets plant exact ties, and include -0.0/+0.0
+            ki = rng.choice(np.array([0.0, -0.0, 1.5, 2.25, -7.0, 3e-8, 1e30], np.float32), size=total)
+            ki = np.where(rng.random(total) < 0.5, ki, rng.standard_normal(total).astype(np.float32))
+            ks = rng.choice(np.array([-1.0, -0.0, 0.0, 0.5, 0.25, 1.0], np.float32), size=total)
+            ks = np.where(rng.random(total) < 0.5, ks, rng.uniform(-1, 1, total).astype(np.float32))
+        elif shape == "const":
+            ki = np.full(total, 0.75, np.float32)
+            ks = np.full(total, -0.125, np.float32)
+        elif shape == "outlier":
+            ki = (0.57 + 1e-4 * rng.standard_normal(total)).astype(np.float32)
+            ki[total // 2] = 4095.0
+            ks = (0.3 + 1e-3 * rng.standard_normal(total)).astype(np.float32)
+            ks[total // 3] = -1.0
+        else:
+            ki = (1.0 + 1e-6 * rng.integers(0, 40, total)).astype(np.float32)
+            ks = (0.5 + 1e-7 * rng.integers(0, 300, total)).astype(np.float32)
         r = tr.Reducer(8, 8, torch.bfloat16, lam=lam, max_images=len(N), max_tokens=total,
                        max_N=max(N))
         idx, src = r.select(torch.from_numpy(ki).to(DEV), torch.from_numpy(ks).to(DEV), N, K)
