@@ -162,8 +162,11 @@ class Reducer:
         return ReduceResult(out, out_idx, out_src, h2, s)
 
     def score(self, X: torch.Tensor, Xpre: torch.Tensor, Xpost: torch.Tensor, *,
-              want_h2: bool = False, stream=None):
-        """Scoring kernel alone: (CV^2 key, s, H2 or None), float32 [rows] each."""
+              want_h2: bool = False, out=None, stream=None):
+        """Scoring kernel alone: (CV^2 key, s, H2 or None), float32 [rows] each.
+
+        ``out`` may pass preallocated (CV^2, s) tensors.
+        """
         self._check_rows("X", X, self.D)
         self._check_rows("Xpre", Xpre, self.Dc)
         self._check_rows("Xpost", Xpost, self.Dc)
@@ -171,7 +174,14 @@ class Reducer:
         if Xpre.shape[0] != rows or Xpost.shape[0] != rows:
             raise ValueError("X, Xpre and Xpost must have the same number of rows")
         f32 = dict(dtype=torch.float32, device=self.device)
-        cv2, s = torch.empty(rows, **f32), torch.empty(rows, **f32)
+        if out is not None:
+            cv2, s = out
+            for t in (cv2, s):
+                if t.dtype != torch.float32 or t.device != self.device or t.dim() != 1 \
+                        or t.numel() != rows or not t.is_contiguous():
+                    raise ValueError("score outputs must be contiguous float32 [rows] tensors")
+        else:
+            cv2, s = torch.empty(rows, **f32), torch.empty(rows, **f32)
         h2 = torch.empty(rows, **f32) if want_h2 else None
         st = self.lib.tr_score(self._ctx, _ptr(X), _ptr(Xpre), _ptr(Xpost), rows, _ptr(cv2),
                                _ptr(s), _ptr(h2), self._stream(stream))
