@@ -31,8 +31,13 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--K", type=int, default=64, choices=[64, 128, 192])
-    ap.add_argument("--images", type=int, default=64)
+    ap.add_argument("--workload", default="llava", choices=["llava", "llava_fp32", "llava_next",
+                                                              "qwen_ragged", "video"],
+                    help="llava (the headline: 64 x 576 x 4096 bf16) or another benchmark "
+                         "workload of the synth module at its full size")
+    ap.add_argument("--K", type=int, default=64, choices=[64, 128, 192],
+                    help="kept tokens per image of the llava workload")
+    ap.add_argument("--images", type=int, default=64, help="images of the llava workload")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="target wall time of the oracle sample")
@@ -63,20 +68,37 @@ def measured_traffic():
     return float(byt.group(1))
 
 
+def describe(w) -> str:
+    n = sorted(set(w.N))
+    ns = str(n[0]) if len(n) == 1 else "%d..%d" % (n[0], n[-1])
+    k = sorted(set(w.K))
+    ks = str(k[0]) if len(k) == 1 else ("%.0f %%" % (100 * w.keep_ratio) if w.keep_ratio else "ragged")
+    kind = {"llava": "llava-1.5 visual tokens", "llava_fp32": "llava-1.5 vision-encoder tokens",
+            "llava_next": "llava-next 5-tile tokens", "qwen_ragged": "dynamic-resolution tokens",
+            "video": "video clips (32 frames)"}[w.name]
+    dt = "bf16" if str(w.dtype).endswith("bfloat16") else "fp32"
+    return "%s, %d x %s tokens x %d %s -> %s kept" % (kind, w.B, ns, w.D, dt, ks)
+
+
 def cpu_baseline(w, seconds: float):
     import oracle
-    X, P, Q = w.X.cpu(), w.Xpre.cpu(), w.Xpost.cpu()
+    # a bounded sample: the first images up to ~40k tokens, repeated to ~`seconds`
+    nb, rows = 0, 0
+    while nb < w.B and (nb == 0 or rows + w.N[nb] <= 40000):
+        rows += w.N[nb]
+        nb += 1
+    X, P, Q = w.X[:rows].cpu(), w.Xpre[:rows].cpu(), w.Xpost[:rows].cpu()
     runs = 0
     t0 = time.perf_counter()
     while True:
-        oracle.reduce(X, P, Q, w.N, w.K, w.lam, want_out=True, want_scores=False)
+        oracle.reduce(X, P, Q, w.N[:nb], w.K[:nb], w.lam, want_out=True, want_scores=False)
         runs += 1
         el = time.perf_counter() - t0
         if el >= seconds or runs >= 50:
             break
-    return {"value": runs * w.B / el, "unit": "images/s", "cores": 1, "kind": "oracle",
-            "sample": "%d x the full %d-image batch (fp64 C oracle, one thread, %.1f s)"
-                      % (runs, w.B, el)}
+    return {"value": runs * nb / el, "unit": "images/s", "cores": 1, "kind": "oracle",
+            "sample": "%d x the first %d of %d images (%d tokens; fp64 C oracle, one thread, %.1f s)"
+                      % (runs, nb, w.B, rows, el)}
 
 
 def main():
@@ -93,9 +115,13 @@ def main():
 
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
-    w = synth.llava(device=dev, B=args.images, N=576, D=4096, K=args.K)
+    if args.workload == "llava":
+        w = synth.llava(device=dev, B=args.images, N=576, D=4096, K=args.K)
+    else:
+        w = synth.make(args.workload, device=dev)
     torch.cuda.synchronize()
-    r = tr.Reducer(w.D, w.Dc, w.dtype, lam=w.lam, max_images=w.B, max_tokens=sum(w.N), max_N=576)
+    r = tr.Reducer(w.D, w.Dc, w.dtype, lam=w.lam, max_images=w.B, max_tokens=sum(w.N),
+                   max_N=max(w.N))
     sk = sum(w.K)
     out = torch.empty(sk, w.D, dtype=w.dtype, device=dev)
     idx = torch.empty(sk, dtype=torch.int32, device=dev)
@@ -152,7 +178,7 @@ def main():
     traffic = measured_traffic()
 
     line = {
-        "metric": METRIC,
+        "metric": METRIC if args.workload == "llava" else "images/s (%s workload)" % args.workload,
         "value": round(images_s, 1),
         "unit": "images/s",
         "n_gpus": 1,
@@ -162,11 +188,10 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        "dtype": "bf16" if w.dtype == torch.bfloat16 else "f32",
         "data": "synthetic",
-        "config": {"workload": "llava-1.5 visual tokens, %d images x 576 tokens x 4096 bf16 -> %d kept"
-                               % (w.B, args.K),
-                   "images": w.B, "tokens_per_image": 576, "D": w.D, "Dc": w.Dc, "K": args.K,
+        "config": {"workload": describe(w),
+                   "images": w.B, "tokens": rows, "D": w.D, "Dc": w.Dc, "kept": sum(w.K),
                    "lambda": round(w.lam, 6)},
         "tokens_per_s": round(rows * args.steps / elapsed, 1),
         "path_hbm": {"algorithmic_bytes": path_bytes,

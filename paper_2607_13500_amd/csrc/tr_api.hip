@@ -178,6 +178,8 @@ struct tr_ctx {
     float* key_imp = nullptr;
     float* key_s = nullptr;
     int32_t* rows = nullptr;
+    uint32_t* gsel = nullptr;     // pick bitmaps of images shared by several workgroups
+    uint32_t* gimp = nullptr;     // their X^imp bitmaps
     bool timing = false;
     std::vector<hipEvent_t> events;   // 4 per timed call
     int timed = 0;
@@ -188,8 +190,8 @@ namespace {
 
 // Launch the selection for every image of a plan (one launch when the batch is
 // uniform, else groups of at most kMaxDescPerLaunch images).
-hipError_t run_select(const Plan& pl, const float* key_imp, const float* key_s, int32_t* out_idx,
-                      uint8_t* out_src, int32_t* out_rows, hipStream_t s)
+hipError_t run_select(const tr_ctx* c, const Plan& pl, const float* key_imp, const float* key_s,
+                      int32_t* out_idx, uint8_t* out_src, int32_t* out_rows, hipStream_t s)
 {
     tr::SelectArgs a;
     memset(&a, 0, sizeof a);
@@ -198,6 +200,8 @@ hipError_t run_select(const Plan& pl, const float* key_imp, const float* key_s, 
     a.out_idx = out_idx;
     a.out_src = out_src;
     a.out_rows = out_rows;
+    a.gsel = c->gsel;
+    a.gimp = c->gimp;
     const int B = (int)pl.desc.size();
     if (B == 0) return hipSuccess;
     if (pl.uniform) {
@@ -205,6 +209,7 @@ hipError_t run_select(const Plan& pl, const float* key_imp, const float* key_s, 
         a.nimg = B;
         a.img0 = 0;
         a.desc[0] = pl.desc[0];
+        a.groups = tr::select_groups(pl.nmax);
         return tr::launch_select(a, pl.nmax, s);
     }
     for (int b0 = 0; b0 < B; b0 += tr::kMaxDescPerLaunch) {
@@ -217,6 +222,7 @@ hipError_t run_select(const Plan& pl, const float* key_imp, const float* key_s, 
             a.desc[i] = pl.desc[(size_t)(b0 + i)];
             if (a.desc[i].n > nmax) nmax = a.desc[i].n;
         }
+        a.groups = tr::select_groups(nmax);
         hipError_t e = tr::launch_select(a, nmax, s);
         if (e != hipSuccess) return e;
     }
@@ -300,11 +306,20 @@ tr_status tr_create(const tr_params* p, tr_ctx** out)
     c->lds_limit = lds;
     c->cap_n = cap;
     const size_t n = (size_t)p->max_tokens;
+    const size_t gw = tr::select_gsel_words(p->max_tokens, p->max_images);
     if ((e = hipMalloc(&c->key_imp, n * sizeof(float))) != hipSuccess ||
         (e = hipMalloc(&c->key_s, n * sizeof(float))) != hipSuccess ||
-        (e = hipMalloc(&c->rows, n * sizeof(int32_t))) != hipSuccess) {
+        (e = hipMalloc(&c->rows, n * sizeof(int32_t))) != hipSuccess ||
+        (e = hipMalloc(&c->gsel, gw * sizeof(uint32_t))) != hipSuccess ||
+        (e = hipMalloc(&c->gimp, gw * sizeof(uint32_t))) != hipSuccess) {
         tr_destroy(c);
         return fail(TR_ENOMEM, "hipMalloc of %zu-token scratch failed: %s", n, hipGetErrorString(e));
+    }
+    // The split selection leaves the pick bitmaps zero after every call.
+    if ((e = hipMemset(c->gsel, 0, gw * sizeof(uint32_t))) != hipSuccess ||
+        (e = hipDeviceSynchronize()) != hipSuccess) {
+        tr_destroy(c);
+        return hip_fail(e, "scratch initialisation");
     }
     if ((e = tr::select_prepare(lds)) != hipSuccess) {
         tr_destroy(c);
@@ -321,6 +336,8 @@ void tr_destroy(tr_ctx* c)
     if (c->key_imp) (void)hipFree(c->key_imp);
     if (c->key_s) (void)hipFree(c->key_s);
     if (c->rows) (void)hipFree(c->rows);
+    if (c->gsel) (void)hipFree(c->gsel);
+    if (c->gimp) (void)hipFree(c->gimp);
     for (hipEvent_t ev : c->events) (void)hipEventDestroy(ev);
     delete c;
 }
@@ -420,7 +437,7 @@ tr_status tr_reduce(tr_ctx* c, const void* X, const void* X_pre, const void* X_p
         return hip_fail(e, "score kernel launch");
     if (ev && (e = hipEventRecord(ev[1], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
 
-    if ((e = run_select(pl, c->key_imp, c->key_s, out_idx, out_src, c->rows, s)) != hipSuccess)
+    if ((e = run_select(c, pl, c->key_imp, c->key_s, out_idx, out_src, c->rows, s)) != hipSuccess)
         return hip_fail(e, "select kernel launch");
     if (ev && (e = hipEventRecord(ev[2], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
 
@@ -481,7 +498,7 @@ tr_status tr_select(tr_ctx* c, const float* key_imp, const float* key_s, int32_t
         return fail(TR_EINVAL, "key and index arrays must be 4-byte aligned");
     DeviceGuard g(c->device);
     if (!g.ok) return fail(TR_EDEVICE, "hipSetDevice(%d) failed", c->device);
-    hipError_t e = run_select(pl, key_imp, key_s, out_idx, out_src, nullptr, static_cast<hipStream_t>(stream));
+    hipError_t e = run_select(c, pl, key_imp, key_s, out_idx, out_src, nullptr, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "select kernel launch");
     return TR_OK;
 }

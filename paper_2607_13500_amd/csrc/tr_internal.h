@@ -48,12 +48,19 @@ struct SelectArgs {
     int32_t* out_idx;       // packed [sum K], image-local
     uint8_t* out_src;       // packed [sum K] or nullptr
     int32_t* out_rows;      // packed [sum K] global row of each kept token, or nullptr
+    uint32_t* gsel;         // per-image pick bitmaps of split images (zero between calls)
+    uint32_t* gimp;         // per-image X^imp bitmaps of split images
     int32_t uniform;        // 1: desc[0] holds n/k1/k2/t of every image
     int32_t nimg;           // images in this launch
-    int32_t img0;           // index of the first image (uniform mode)
-    int32_t pad;
+    int32_t img0;           // index of the first image of this launch in the batch
+    int32_t groups;         // workgroups per image (1, or more to split large images)
     ImageDesc desc[kMaxDescPerLaunch];
 };
+
+// Words of the split-image pick bitmaps for capacity (max_tokens, max_images).
+size_t select_gsel_words(int64_t max_tokens, int max_images);
+// Workgroups per image for a launch whose largest image has nmax tokens.
+int select_groups(int nmax);
 
 // Threads per selection workgroup for images of at most nmax tokens.
 int select_threads(int nmax);

@@ -14,18 +14,16 @@
 // stops when
 //   - the bucket holds a single key value T: keys < T are kept, then the first
 //     keys == T in token order (ordered ballot counts), or
-//   - (images of at most 4096 tokens) the bucket holds at most 128 keys: each
-//     bucket member counts the members smaller than itself in (key, index)
-//     order, exactly, and is kept if that rank is below the remaining budget.
-// Stage II (images of at most 4096 tokens): one bucketing pass, 256 buckets of
-// equal width over the [min, max] of X^rem's keys, places X^rem in bucket
-// order; every token then counts the members of its own bucket smaller in
-// (key, index) order, so its rank in the sorted X^rem is exact.  If a bucket
-// exceeds 128 tokens, the range is not finite, (or
-// for larger images) Stage II falls back to a 4-pass stable LSD radix sort of
-// the 16-bit indices of X^rem (ordered compaction first, digits looked up by
-// index, per-wavefront scatter offsets), with passes over constant bytes
-// skipped.
+//   - the bucket holds at most 128 keys: each bucket member counts the members
+//     smaller than itself in (key, index) order, exactly, and is kept if that
+//     rank is below the remaining budget.
+// Stage II buckets X^rem by value, 1024 buckets of equal width over the
+// [min, max] of its keys, in one pass; every token then counts the members of
+// its own bucket smaller in (key, index) order, so its rank in the sorted
+// X^rem is exact.  If a bucket exceeds 256 tokens or the range is not finite,
+// Stage II falls back to a stable LSD radix sort of the 16-bit indices of
+// X^rem (ordered compaction first, digits looked up by index, per-wavefront
+// scatter offsets, passes over constant bytes skipped).
 //
 // Every wavefront owns a contiguous, 64-aligned range of tokens for the
 // ordered steps (tie marking, compaction, output), so all results are exact
@@ -38,27 +36,34 @@ namespace {
 
 constexpr int kThreads = 1024;
 constexpr int kW = kThreads / kWave;
-constexpr int kSmallMaxN = 4096;
-constexpr uint32_t kCountLimit = 128;
+constexpr uint32_t kCountLimit = 128;    // Stage I: count exactly inside buckets this small
+constexpr int kBuckets = kThreads;       // Stage II: value buckets (one per thread in the scan)
+constexpr uint32_t kBucketLimit = 256;   // Stage II: largest bucket ranked by counting
+constexpr int kDenseRem = 4096;          // Stage II: rank whole buckets per wavefront from here
+constexpr int kSplitGroups = 16;         // workgroups sharing the ranking of one large image
 
 // ---- LDS layout (same arithmetic on host and device) -----------------------
 struct LdsLayout {
-    size_t ks, ki, list, bimp, bsel, hsh, cur, hist, slots, misc, total;
+    size_t ks, ki, bimp, bsel, area, slots, misc, total;
 };
 
 __host__ __device__ inline size_t align_up(size_t v, size_t a) { return (v + a - 1) & ~(a - 1); }
 
 //   ks    u32[n]        Stage II keys by token index
-//   ki    u32[n]        Stage I keys; after Stage I two u16[n] index buffers
-//   list  u64[n]        (key << 16 | index) of bucket members (small images)
+//   ki    u32[n]        Stage I keys; after Stage I the same bytes hold the
+//                       u16 bucket list of X^rem, or the two u16[n] index
+//                       buffers of the radix sort
 //   bimp  u32[nw]       X^imp bitmap (nw = 2 ceil(n / 64))
 //   bsel  u32[nw]       X^imp U X^div bitmap
-//   hsh   u32[2][256]   digit histograms (double buffered), 16-byte aligned
-//   cur   u32[256]      bucket cursors (small images)
-//   hist  u16[256][W]   per-wavefront digit counts / offsets of the LSD sort
-//   slots u32[8][W]     per-wavefront partial counts, one row per use
+//   area  u32[2048]     16-byte aligned, reused by phase:
+//                         Stage I:  [0, 512) two 256-bin digit histograms,
+//                                   [512, 768) u64[128] bucket members
+//                         Stage II: [0, 1024) bucket counts, [1024, 2048)
+//                                   bucket cursors; or u16[256][W] digit
+//                                   counts / offsets of the radix sort
+//   slots u32[8][W]     per-wavefront partial values, one row per use
 //   misc  u32[16]       broadcast slots and counters
-__host__ __device__ inline LdsLayout lds_layout(int n, bool small)
+__host__ __device__ inline LdsLayout lds_layout(int n)
 {
     LdsLayout L;
     const size_t nw = 2 * (((size_t)n + 63) / 64);
@@ -67,20 +72,13 @@ __host__ __device__ inline LdsLayout lds_layout(int n, bool small)
     o += 4 * (size_t)n;
     L.ki = o;
     o += 4 * (size_t)n;
-    o = align_up(o, 8);
-    L.list = o;
-    if (small) o += 8 * (size_t)n;
     L.bimp = o;
     o += 4 * nw;
     L.bsel = o;
     o += 4 * nw;
     o = align_up(o, 16);
-    L.hsh = o;
-    o += 4 * 512;
-    L.cur = o;
-    if (small) o += 4 * 256;
-    L.hist = o;
-    o += 2 * 256 * kW;
+    L.area = o;
+    o += 4 * 2048;
     L.slots = o;
     o += 4 * 8 * kW;
     L.misc = o;
@@ -95,6 +93,12 @@ __device__ __forceinline__ uint32_t order_key(float f)
 {
     const uint32_t u = __float_as_uint(f + 0.0f);
     return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// Inverse of order_key.
+__device__ __forceinline__ float key_value(uint32_t k)
+{
+    return __uint_as_float((k & 0x80000000u) ? (k ^ 0x80000000u) : ~k);
 }
 
 __device__ __forceinline__ uint64_t lanes_below(int lane) { return (1ull << lane) - 1ull; }
@@ -151,16 +155,16 @@ struct Img {
     int row_off, n, k1, k2, t, out_off;
 };
 
-__device__ __forceinline__ Img image_of(const SelectArgs& a)
+__device__ __forceinline__ Img image_of(const SelectArgs& a, int local)
 {
     ImageDesc d;
     if (a.uniform) {
         d = a.desc[0];
-        const int img = a.img0 + (int)blockIdx.x;
+        const int img = a.img0 + local;
         d.row_off = img * d.n;
         d.out_off = img * (d.k1 + d.k2);
     } else {
-        d = a.desc[blockIdx.x];
+        d = a.desc[local];
     }
     return Img{d.row_off, d.n, d.k1, d.k2, d.t, d.out_off};
 }
@@ -171,13 +175,13 @@ __device__ __forceinline__ Img image_of(const SelectArgs& a)
 // differs from token 0's key.
 __device__ void load_keys(const SelectArgs& a, const Img& d, uint32_t* ki, uint32_t* ks,
                           uint32_t* zero, int nzero, uint32_t* slots, uint32_t& k0i,
-                          uint32_t& VI, uint32_t& VS)
+                          uint32_t& VI, uint32_t& VS, uint32_t& kimin, uint32_t& kimax)
 {
     const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
     const int N = d.n;
     k0i = order_key(a.key_imp[d.row_off]);
     const uint32_t k0s = order_key(a.key_s[d.row_off]);
-    uint32_t vi = 0, vs = 0;
+    uint32_t vi = 0, vs = 0, nlo = 0, hi = 0;
     for (int i0 = tid; i0 < N; i0 += 4 * kThreads) {
         float fi[4], fs[4];
 #pragma unroll
@@ -197,23 +201,35 @@ __device__ void load_keys(const SelectArgs& a, const Img& d, uint32_t* ki, uint3
                 ks[i] = qs;
                 vi |= qi ^ k0i;
                 vs |= qs ^ k0s;
+                nlo = max(nlo, ~qi);
+                hi = max(hi, qi);
             }
         }
     }
     for (int i = tid; i < nzero; i += kThreads) zero[i] = 0;
     vi = wave_or_u32(vi);
     vs = wave_or_u32(vs);
+    nlo = wave_max_u32(nlo);
+    hi = wave_max_u32(hi);
     if (lane == 0) {
         slots[w] = vi;
         slots[kW + w] = vs;
+        slots[2 * kW + w] = nlo;
+        slots[3 * kW + w] = hi;
     }
     __syncthreads();
     VI = 0;
     VS = 0;
+    nlo = 0;
+    hi = 0;
     for (int i = 0; i < kW; ++i) {
         VI |= slots[i];
         VS |= slots[kW + i];
+        nlo = max(nlo, slots[2 * kW + i]);
+        hi = max(hi, slots[3 * kW + i]);
     }
+    kimin = ~nlo;
+    kimax = hi;
 }
 
 // Stage I digit passes (see the file comment).  On return the bucket
@@ -270,6 +286,87 @@ __device__ void stage1_narrow(const uint32_t* ki, int N, uint32_t VI, uint32_t* 
         m = misc[2];
         pmask |= win;
     }
+}
+
+// Value bucket of a key: floor((v - fmin) * scale) clamped to the last
+// bucket, non-decreasing in the key.
+__device__ __forceinline__ int value_bucket(uint32_t key, float fmin, float scale)
+{
+    return min(kBuckets - 1, (int)((key_value(key) - fmin) * scale));
+}
+
+// Stage I by one bucketing pass: 1024 buckets of equal width over the key
+// range; tokens in buckets below the one holding the K1-th key are kept, and
+// members of that bucket (at most kCountLimit of them) are kept when fewer
+// than the remaining budget of members precede them in (key, index) order.
+// H (kBuckets words) must be zero; list holds kCountLimit u64; misc[8] must be
+// 0.  Returns false (having written only H, misc[0..2] and `row`) when the
+// range is not finite or the boundary bucket is larger.
+__device__ bool stage1_bucket(const uint32_t* ki, int N, uint32_t K1, uint32_t kimin, uint32_t kimax,
+                              uint32_t* H, uint64_t* list, uint32_t* misc, uint32_t* row,
+                              uint32_t* bimp, uint32_t* bsel)
+{
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
+    int beg, end;
+    wave_range(N, w, beg, end);
+    const float fmin = key_value(kimin);
+    const float width = key_value(kimax) - fmin;
+    if (!(width > 0.f) || !(width < 3.0e38f)) return false;
+    const float scale = (float)kBuckets / width;
+    for (int base = beg; base < end; base += kWave) {
+        const int i = base + lane;
+        if (i < end) atomicAdd(&H[value_bucket(ki[i], fmin, scale)], 1u);
+    }
+    __syncthreads();
+    {   // thread tid owns bucket tid: find the bucket holding the K1-th key
+        const uint32_t c = H[tid];
+        const uint32_t inc = wave_scan_add(c);
+        if (lane == kWave - 1) row[w] = inc;
+        __syncthreads();
+        uint32_t start = inc - c;
+        for (int i = 0; i < w; ++i) start += row[i];
+        if (start < K1 && K1 <= start + c) {
+            misc[0] = (uint32_t)tid;
+            misc[1] = K1 - start;
+            misc[2] = c;
+        }
+    }
+    __syncthreads();
+    const int dstar = (int)misc[0];
+    const uint32_t need = misc[1];
+    if (misc[2] > kCountLimit) return false;
+    for (int base = beg; base < end; base += kWave) {
+        const int i = base + lane;
+        const uint32_t key = i < end ? ki[i] : 0u;
+        const bool member = i < end && value_bucket(key, fmin, scale) == dstar;
+        const uint64_t bm = __ballot(member);
+        if (bm) {
+            const int leader = (int)__ffsll((long long)bm) - 1;
+            uint32_t b0 = 0;
+            if (lane == leader) b0 = atomicAdd(&misc[8], (uint32_t)__popcll(bm));
+            b0 = (uint32_t)__builtin_amdgcn_readlane((int)b0, leader);
+            if (member) list[b0 + __popcll(bm & lanes_below(lane))] = ((uint64_t)key << 16) | (uint32_t)i;
+        }
+    }
+    __syncthreads();
+    const uint32_t m = misc[8];
+    for (int base = beg; base < end; base += kWave) {
+        const int i = base + lane;
+        const bool act = i < end;
+        const uint32_t key = act ? ki[i] : 0u;
+        const int dg = act ? value_bucket(key, fmin, scale) : kBuckets;
+        bool take = act && dg < dstar;
+        if (act && dg == dstar) {
+            const uint64_t mine = ((uint64_t)key << 16) | (uint32_t)i;
+            uint32_t r = 0;
+            for (uint32_t j = 0; j < m; ++j) r += list[j] < mine ? 1u : 0u;
+            take = r < need;
+        }
+        const uint64_t bt = __ballot(take);
+        put_tile_bits(bimp, base, bt, lane);
+        put_tile_bits(bsel, base, bt, lane);
+    }
+    return true;
 }
 
 // Stage I marking with a resolved threshold key T: keys < T, then the first
@@ -344,23 +441,24 @@ __device__ void stage1_mark_counted(const uint32_t* ki, int N, uint32_t prefix, 
     }
 }
 
-// Inverse of order_key.
-__device__ __forceinline__ float key_value(uint32_t k)
-{
-    return __uint_as_float((k & 0x80000000u) ? (k ^ 0x80000000u) : ~k);
-}
-
 // Stage II by one bucketing pass and exact counting inside buckets.  Bucket
-// d of a remaining token is floor((s - s_min) * 256 / (s_max - s_min)) over
-// the remainder's key range, a non-decreasing function of s in fp32 (every
-// step rounds monotonically), so bucket order agrees with key order and the
-// exact (key, index) count inside a bucket gives the exact rank.  H (256
-// words) must be zero.  Returns false, having changed nothing but H, cur,
-// list and misc[3..5], when a bucket holds more than kCountLimit tokens or
-// the range is not finite.
-__device__ bool stage2_bucket(const uint32_t* ks, const uint32_t* bimp, uint32_t* bsel, int N,
-                              int K2, int t, uint32_t* H, uint32_t* cur, uint64_t* list,
-                              uint32_t* misc, uint32_t* row_lo, uint32_t* row_hi, uint32_t* row)
+// d of a remaining token is floor((s - s_min) * B / (s_max - s_min)) (B =
+// 1024 buckets over the remainder's key range), a non-decreasing function of s
+// in fp32 (every step rounds monotonically), so bucket order agrees with key
+// order and counting inside a bucket the members smaller in (key, index)
+// order gives the exact rank.  `list` receives the indices of X^rem in bucket
+// order (n u16).  H (B words) must be zero.  Returns false, having written
+// only H, cur, list and slot rows, when a bucket holds more than kBucketLimit
+// tokens or the key range is not finite.
+// Result of stage2_bucket.
+constexpr int kS2Failed = 0;   // nothing decided: sort instead
+constexpr int kS2Local = 1;    // every pick is in bsel
+constexpr int kS2Global = 2;   // this group's picks are in the global bitmap
+
+__device__ int stage2_bucket(const uint32_t* ks, const uint32_t* bimp, uint32_t* bsel, int N,
+                              int R, int K2, int t, uint32_t* H, uint32_t* cur, uint16_t* list,
+                              uint32_t* row_lo, uint32_t* row_hi, uint32_t* row_a, uint32_t* row_b,
+                              int part, int parts, uint32_t* gpick)
 {
     const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
     int beg, end;
@@ -397,7 +495,7 @@ __device__ bool stage2_bucket(const uint32_t* ks, const uint32_t* bimp, uint32_t
             const int i = base + lane;
             rc += __popcll(__ballot(i < end && !bit_of(bimp, i)));
         }
-        uint32_t r0 = wave_prefix(rc, row);
+        uint32_t r0 = wave_prefix(rc, row_a);
         for (int base = beg; base < end; base += kWave) {
             const int i = base + lane;
             const bool rem = i < end && !bit_of(bimp, i);
@@ -408,66 +506,120 @@ __device__ bool stage2_bucket(const uint32_t* ks, const uint32_t* bimp, uint32_t
             if (lane == 32) bsel[(base >> 5) + 1] = bimp[(base >> 5) + 1] | (uint32_t)(bp >> 32);
             r0 += (uint32_t)__popcll(br);
         }
-        return true;
+        return kS2Local;
     }
     const float fmin = key_value(kmin);
     const float width = key_value(kmax) - fmin;
-    if (!(width > 0.f) || !(width < 3.0e38f)) return false;   // not finite: sort instead
-    const float scale = 256.f / width;
+    if (!(width > 0.f) || !(width < 3.0e38f)) return kS2Failed;   // not finite: sort instead
+    const float scale = (float)kBuckets / width;
 
     for (int base = beg; base < end; base += kWave) {
         const int i = base + lane;
-        const bool rem = i < end && !bit_of(bimp, i);
-        uint32_t dg = 0;
-        if (rem) dg = (uint32_t)min(255, (int)((key_value(ks[i]) - fmin) * scale));
-        const uint64_t mm = same_digit(dg, rem);
-        if (rem && is_leader(mm, lane)) atomicAdd(&H[dg], (uint32_t)__popcll(mm));
+        if (i < end && !bit_of(bimp, i)) {
+            const int dg = value_bucket(ks[i], fmin, scale);
+            atomicAdd(&H[dg], 1u);
+        }
     }
     __syncthreads();
-    if (w == 0) {
-        const uint4 c4 = *reinterpret_cast<const uint4*>(H + lane * 4);
-        const uint32_t sum = c4.x + c4.y + c4.z + c4.w;
-        const uint32_t start = wave_scan_add(sum) - sum;
-        *reinterpret_cast<uint4*>(cur + lane * 4) =
-            make_uint4(start, start + c4.x, start + c4.x + c4.y, start + c4.x + c4.y + c4.z);
-        const uint32_t mx = wave_max_u32(max(max(c4.x, c4.y), max(c4.z, c4.w)));
-        if (lane == 0) misc[3] = mx;
+    {   // exclusive bucket starts and the largest bucket; thread tid owns bucket tid
+        const uint32_t c = H[tid];
+        const uint32_t inc = wave_scan_add(c);
+        const uint32_t mx = wave_max_u32(c);
+        if (lane == kWave - 1) row_a[w] = inc;
+        if (lane == 0) row_b[w] = mx;
+        __syncthreads();
+        uint32_t start = inc - c, big = 0;
+        for (int i = 0; i < kW; ++i) {
+            if (i < w) start += row_a[i];
+            big = max(big, row_b[i]);
+        }
+        cur[tid] = start;
+        if (big > kBucketLimit) return kS2Failed;   // the same decision in every thread
     }
     __syncthreads();
-    if (misc[3] > kCountLimit) return false;
     for (int base = beg; base < end; base += kWave) {
         const int i = base + lane;
-        const bool rem = i < end && !bit_of(bimp, i);
-        const uint32_t key = rem ? ks[i] : 0u;
-        uint32_t dg = 0;
-        if (rem) dg = (uint32_t)min(255, (int)((key_value(key) - fmin) * scale));
-        const uint64_t mm = same_digit(dg, rem);
-        const int leader = mm ? (int)__ffsll((long long)mm) - 1 : lane;
-        uint32_t b0 = 0;
-        if (rem && leader == lane) b0 = atomicAdd(&cur[dg], (uint32_t)__popcll(mm));
-        b0 = (uint32_t)__shfl((int)b0, leader, kWave);
-        if (rem) list[b0 + __popcll(mm & lanes_below(lane))] = ((uint64_t)key << 16) | (uint32_t)i;
+        if (i < end && !bit_of(bimp, i)) {
+            const int dg = value_bucket(ks[i], fmin, scale);
+            list[atomicAdd(&cur[dg], 1u)] = (uint16_t)i;
+        }
     }
     __syncthreads();
+    if (R >= kDenseRem) {
+        // Dense buckets: a wavefront ranks a whole bucket at a time.  Members
+        // sit in lanes (64 per chunk) and every member of the bucket is
+        // broadcast from its lane, so each member is read from LDS once.
+        // With `parts` workgroups on the image, bucket q belongs to the
+        // wavefront numbered q % (parts W) across them (lane q / (parts W));
+        // picks then go to the image's global bitmap gpick.
+        const int waves = parts * kW;
+        const int q = part * kW + w + waves * lane;
+        const bool mine = q < kBuckets;
+        const uint32_t cnt = mine ? H[q] : 0u;
+        const uint32_t stop = mine ? cur[q] : 0u;
+        uint64_t todo = __ballot(cnt > 0);
+        while (todo) {
+            const int l = (int)__ffsll((long long)todo) - 1;
+            todo &= todo - 1;
+            const uint32_t b = (uint32_t)__builtin_amdgcn_readlane((int)cnt, l);
+            const uint32_t start = (uint32_t)__builtin_amdgcn_readlane((int)stop, l) - b;
+            for (uint32_t c0 = 0; c0 < b; c0 += kWave) {
+                const bool have = c0 + lane < b;
+                const uint32_t myid = have ? list[start + c0 + lane] : 0u;
+                const uint32_t mykey = have ? ks[myid] : 0u;
+                uint32_t r = 0;
+                for (uint32_t c1 = 0; c1 < b; c1 += kWave) {
+                    uint32_t oid = myid, okey = mykey;
+                    if (c1 != c0) {
+                        const bool oh = c1 + lane < b;
+                        oid = oh ? list[start + c1 + lane] : 0u;
+                        okey = oh ? ks[oid] : 0u;
+                    }
+                    const uint32_t n1 = min((uint32_t)kWave, b - c1);
+                    for (uint32_t j = 0; j < n1; ++j) {
+                        const uint32_t kj = (uint32_t)__builtin_amdgcn_readlane((int)okey, (int)j);
+                        const uint32_t ij = (uint32_t)__builtin_amdgcn_readlane((int)oid, (int)j);
+                        r += (kj < mykey || (kj == mykey && ij < myid)) ? 1u : 0u;
+                    }
+                }
+                const uint32_t rr = start + r;
+                if (have && rr % (uint32_t)t == 0 && rr < span) {
+                    if (gpick) atomicOr(&gpick[myid >> 5], 1u << (myid & 31));
+                    else atomicOr(&bsel[myid >> 5], 1u << (myid & 31));
+                }
+            }
+        }
+        return gpick ? kS2Global : kS2Local;
+    }
     for (int base = beg; base < end; base += kWave) {
         const int i = base + lane;
         const bool rem = i < end && !bit_of(bimp, i);
         bool picked = false;
         if (rem) {
             const uint32_t key = ks[i];
-            const uint32_t dg = (uint32_t)min(255, (int)((key_value(key) - fmin) * scale));
+            const int dg = value_bucket(key, fmin, scale);
             const uint32_t stop = cur[dg];
-            const uint32_t start = stop - H[dg];
-            const uint64_t mine = ((uint64_t)key << 16) | (uint32_t)i;
-            uint32_t r = start;
-            for (uint32_t j = start; j < stop; ++j) r += list[j] < mine ? 1u : 0u;
+            uint32_t j = stop - H[dg];
+            uint32_t r = j;
+            for (; j + 4 <= stop; j += 4) {
+                const uint32_t i0 = list[j], i1 = list[j + 1], i2 = list[j + 2], i3 = list[j + 3];
+                const uint32_t k0 = ks[i0], k1 = ks[i1], k2 = ks[i2], k3 = ks[i3];
+                r += (k0 < key || (k0 == key && i0 < (uint32_t)i)) ? 1u : 0u;
+                r += (k1 < key || (k1 == key && i1 < (uint32_t)i)) ? 1u : 0u;
+                r += (k2 < key || (k2 == key && i2 < (uint32_t)i)) ? 1u : 0u;
+                r += (k3 < key || (k3 == key && i3 < (uint32_t)i)) ? 1u : 0u;
+            }
+            for (; j < stop; ++j) {
+                const uint32_t ij = list[j], kj = ks[ij];
+                r += (kj < key || (kj == key && ij < (uint32_t)i)) ? 1u : 0u;
+            }
             picked = r % (uint32_t)t == 0 && r < span;
         }
         const uint64_t bp = __ballot(picked);
         if (lane == 0) bsel[base >> 5] = bimp[base >> 5] | (uint32_t)bp;
         if (lane == 32) bsel[(base >> 5) + 1] = bimp[(base >> 5) + 1] | (uint32_t)(bp >> 32);
     }
-    return true;
+    return kS2Local;
 }
 
 // Stage II by ordered compaction and a stable LSD radix sort of 16-bit
@@ -576,63 +728,123 @@ __device__ void emit(const SelectArgs& a, const Img& d, const uint32_t* bimp, co
     }
 }
 
-template <bool SMALL>
 __global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a)
 {
     extern __shared__ __align__(16) unsigned char smem[];
-    const Img d = image_of(a);
+    const int G = a.groups > 0 ? a.groups : 1;
+    const int local = (int)blockIdx.x / G, part = (int)blockIdx.x % G;
+    const int img = a.img0 + local;
+    const Img d = image_of(a, local);
     const int N = d.n, K1 = d.k1, K2 = d.k2;
-    const LdsLayout L = lds_layout(N, SMALL);
+    // A large image is shared by G workgroups: each repeats the deterministic
+    // Stage I and bucketing in its own LDS and ranks 1/G of the buckets into
+    // the image's global pick bitmap; emit_kernel then writes the output.
+    const bool split = G > 1 && K2 > 0 && N - K1 >= kDenseRem;
+    if (part > 0 && !split) return;
+    const LdsLayout L = lds_layout(N);
     uint32_t* ks = reinterpret_cast<uint32_t*>(smem + L.ks);
     uint32_t* ki = reinterpret_cast<uint32_t*>(smem + L.ki);
-    uint64_t* list = reinterpret_cast<uint64_t*>(smem + L.list);
     uint32_t* bimp = reinterpret_cast<uint32_t*>(smem + L.bimp);
     uint32_t* bsel = reinterpret_cast<uint32_t*>(smem + L.bsel);
-    uint32_t* hsh = reinterpret_cast<uint32_t*>(smem + L.hsh);
-    uint32_t* cur = reinterpret_cast<uint32_t*>(smem + L.cur);
-    uint16_t* hist = reinterpret_cast<uint16_t*>(smem + L.hist);
+    uint32_t* area = reinterpret_cast<uint32_t*>(smem + L.area);
     uint32_t* slots = reinterpret_cast<uint32_t*>(smem + L.slots);
     uint32_t* misc = reinterpret_cast<uint32_t*>(smem + L.misc);
     const int nw = 2 * ((N + 63) / 64);
 
-    // hsh (512 words) and misc (16 words) start at zero
-    uint32_t k0i, VI, VS;
+    // Slot rows (each written, then read after a barrier, then not touched
+    // again until further barriers have passed): 0-3 key ranges and varying
+    // bits, 4 Stage I scans, 5 Stage I tie ranks, 6-7 Stage II ranges, 2-3
+    // Stage II scans, 4-5 the radix sort, 6 the output offsets.
+    uint32_t k0i, VI, VS, kimin, kimax;
     if (threadIdx.x < 16) misc[threadIdx.x] = 0;
-    load_keys(a, d, ki, ks, hsh, 512, slots, k0i, VI, VS);
+    load_keys(a, d, ki, ks, area, kBuckets, slots, k0i, VI, VS, kimin, kimax);
 
     // ---- Stage I ---------------------------------------------------------------
+    uint64_t* list1 = reinterpret_cast<uint64_t*>(area + kBuckets);   // kCountLimit u64
     if (K1 == 0 || K1 == N) {
         const uint32_t fill = K1 ? 0xffffffffu : 0u;
         for (int i = threadIdx.x; i < nw; i += kThreads) {
             bimp[i] = fill;
             bsel[i] = fill;
         }
-    } else {
+    } else if (kimin == kimax) {   // every key is equal: the first K1 tokens
+        stage1_mark_resolved(ki, N, kimin, (uint32_t)K1, bimp, bsel, slots + 5 * kW);
+    } else if (!stage1_bucket(ki, N, (uint32_t)K1, kimin, kimax, area, list1, misc, slots + 4 * kW,
+                              bimp, bsel)) {
+        __syncthreads();   // everyone is past the bucket attempt: reset its scratch
+        area[threadIdx.x] = 0;
+        if (threadIdx.x < 16) misc[threadIdx.x] = 0;
+        __syncthreads();
         uint32_t prefix = k0i & ~VI, pmask = ~VI, need = (uint32_t)K1, m = (uint32_t)N;
         bool resolved;
-        stage1_narrow(ki, N, VI, hsh, misc, SMALL ? kCountLimit : 0u, prefix, pmask, need, m, resolved);
-        if (resolved) stage1_mark_resolved(ki, N, prefix, need, bimp, bsel, slots + 2 * kW);
-        else stage1_mark_counted(ki, N, prefix, pmask, need, list, misc, bimp, bsel);
+        stage1_narrow(ki, N, VI, area, misc, kCountLimit, prefix, pmask, need, m, resolved);
+        if (resolved) stage1_mark_resolved(ki, N, prefix, need, bimp, bsel, slots + 5 * kW);
+        else stage1_mark_counted(ki, N, prefix, pmask, need, list1, misc, bimp, bsel);
     }
-    __syncthreads();   // the Stage I histograms are read no more; ki is dead
-    // hsh's first 256 words become the Stage II histogram
-    if (threadIdx.x < 256) hsh[threadIdx.x] = 0;
+    __syncthreads();   // Stage I's histograms and list are read no more; ki is dead
+    area[threadIdx.x] = 0;   // Stage II bucket counts
     __syncthreads();
 
     // ---- Stage II --------------------------------------------------------------
     if (K2 > 0) {
-        bool done = false;
-        if (SMALL)
-            done = stage2_bucket(ks, bimp, bsel, N, K2, d.t, hsh, cur, list, misc, slots + 3 * kW,
-                                 slots + 7 * kW, slots + 1 * kW);
-        if (!done) {
-            uint16_t* idx_a = reinterpret_cast<uint16_t*>(ki);
-            stage2_radix(ks, bimp, bsel, N, K1, K2, d.t, VS, idx_a, idx_a + N, hist, slots + 4 * kW,
-                         slots + 5 * kW);
+        uint16_t* idx = reinterpret_cast<uint16_t*>(ki);
+        const size_t wbase = (size_t)(d.row_off >> 5) + 2 * (size_t)img;
+        uint32_t* gpick = split ? a.gsel + wbase : nullptr;
+        int st = stage2_bucket(ks, bimp, bsel, N, N - K1, K2, d.t, area, area + kBuckets, idx,
+                               slots + 6 * kW, slots + 7 * kW, slots + 2 * kW, slots + 3 * kW,
+                               split ? part : 0, split ? G : 1, gpick);
+        if (st == kS2Failed) {
+            if (part > 0) return;   // the same decision in every group: group 0 sorts
+            __syncthreads();        // every thread is past the bucket attempt
+            stage2_radix(ks, bimp, bsel, N, K1, K2, d.t, VS, idx, idx + N,
+                         reinterpret_cast<uint16_t*>(area), slots + 4 * kW, slots + 5 * kW);
+            st = kS2Local;
+        }
+        if (split) {
+            // The output of a shared image is written by emit_kernel after this
+            // launch: group 0 publishes X^imp (and picks it made alone).
+            if (part == 0) {
+                __syncthreads();
+                for (int i = threadIdx.x; i < (N + 31) / 32; i += kThreads) {
+                    a.gimp[wbase + i] = bimp[i];
+                    if (st == kS2Local) {
+                        const uint32_t extra = bsel[i] & ~bimp[i];
+                        if (extra) atomicOr(&gpick[i], extra);
+                    }
+                }
+            }
+            return;
         }
     }
     __syncthreads();
     emit(a, d, bimp, bsel, slots + 6 * kW);
+}
+
+// Output of the images select_kernel shared between workgroups: X^imp and the
+// picks from the global bitmaps (which are cleared for the next call), then
+// the ordered output.  One workgroup per image of the launch.
+__global__ __launch_bounds__(kThreads) void emit_kernel(SelectArgs a)
+{
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int G = a.groups > 0 ? a.groups : 1;
+    const int local = (int)blockIdx.x;
+    const int img = a.img0 + local;
+    const Img d = image_of(a, local);
+    const int N = d.n, K1 = d.k1, K2 = d.k2;
+    if (!(G > 1 && K2 > 0 && N - K1 >= kDenseRem)) return;   // emitted by select_kernel
+    const int nw = 2 * ((N + 63) / 64);
+    uint32_t* bimp = reinterpret_cast<uint32_t*>(smem);
+    uint32_t* bsel = bimp + nw;
+    uint32_t* slots = bsel + nw;
+    const size_t wbase = (size_t)(d.row_off >> 5) + 2 * (size_t)img;
+    for (int i = threadIdx.x; i < (N + 31) / 32; i += kThreads) {
+        const uint32_t im = a.gimp[wbase + i];
+        bimp[i] = im;
+        bsel[i] = im | a.gsel[wbase + i];
+        a.gsel[wbase + i] = 0u;
+    }
+    __syncthreads();
+    emit(a, d, bimp, bsel, slots);
 }
 
 }  // namespace
@@ -643,30 +855,41 @@ int select_threads(int nmax)
     return kThreads;
 }
 
+int select_groups(int nmax)
+{
+    return nmax >= kDenseRem ? kSplitGroups : 1;
+}
+
+size_t select_gsel_words(int64_t max_tokens, int max_images)
+{
+    return (size_t)(max_tokens / 32) + 2 * (size_t)max_images + 2;
+}
+
 size_t select_lds_bytes(int n, int threads)
 {
     (void)threads;
-    return lds_layout(n, n <= kSmallMaxN).total;
+    return lds_layout(n).total;
 }
 
 hipError_t select_prepare(int lds_limit)
 {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&select_kernel<false>),
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&select_kernel),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, lds_limit);
     if (e != hipSuccess) return e;
-    return hipFuncSetAttribute(reinterpret_cast<const void*>(&select_kernel<true>),
+    return hipFuncSetAttribute(reinterpret_cast<const void*>(&emit_kernel),
                                hipFuncAttributeMaxDynamicSharedMemorySize, lds_limit);
 }
 
 hipError_t launch_select(const SelectArgs& a, int nmax, hipStream_t s)
 {
     if (a.nimg <= 0) return hipSuccess;
-    const bool small = nmax <= kSmallMaxN;
-    const size_t lds = lds_layout(nmax, small).total;
-    if (small)
-        hipLaunchKernelGGL(select_kernel<true>, dim3(a.nimg), dim3(kThreads), lds, s, a);
-    else
-        hipLaunchKernelGGL(select_kernel<false>, dim3(a.nimg), dim3(kThreads), lds, s, a);
+    const size_t lds = lds_layout(nmax).total;
+    const int groups = a.groups > 0 ? a.groups : 1;
+    hipLaunchKernelGGL(select_kernel, dim3(a.nimg * groups), dim3(kThreads), lds, s, a);
+    if (groups > 1) {
+        const size_t elds = 8 * (2 * (((size_t)nmax + 63) / 64)) + 4 * 8 * kW;
+        hipLaunchKernelGGL(emit_kernel, dim3(a.nimg), dim3(kThreads), elds, s, a);
+    }
     return hipGetLastError();
 }
 
