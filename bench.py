@@ -38,6 +38,12 @@ def parse():
     ap.add_argument("--K", type=int, default=64, choices=[64, 128, 192],
                     help="kept tokens per image of the llava workload")
     ap.add_argument("--images", type=int, default=64, help="images of the llava workload")
+    ap.add_argument("--lam", type=float, default=None,
+                    help="balance factor lambda (default 1/3, the paper's setting); 1 and 0 are "
+                         "the ablations without the diversity / importance stage, which skip "
+                         "the score they do not use")
+    ap.add_argument("--stride-real", action="store_true",
+                    help="real-interval variant of the diversity stride")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="target wall time of the oracle sample")
@@ -119,16 +125,27 @@ def main():
         w = synth.llava(device=dev, B=args.images, N=576, D=4096, K=args.K)
     else:
         w = synth.make(args.workload, device=dev)
+    if args.lam is not None:
+        w.lam = float(args.lam)
+    headline = (args.workload == "llava" and args.images == 64 and args.K == 64
+                and w.lam == synth.LAMBDA and not args.stride_real)
     torch.cuda.synchronize()
     r = tr.Reducer(w.D, w.Dc, w.dtype, lam=w.lam, max_images=w.B, max_tokens=sum(w.N),
-                   max_N=max(w.N))
+                   max_N=max(w.N), stride_real=args.stride_real)
+    # Which scores the plan needs (the library decides the same way): H2 unless
+    # lambda = 0, s unless lambda = 1.  A score that is not needed is not read.
+    plan = tr.plan(w.N, w.K, w.lam)
+    need_x = any(0 < k1 < n for n, k1 in zip(w.N, plan[1]))
+    need_s = any(0 < k2 < n - k1 for n, k1, k2 in zip(w.N, plan[1], plan[2]))
+    states = (w.Xpre, w.Xpost) if need_s else (None, None)
+    xs = w.X if need_x else None
     sk = sum(w.K)
     out = torch.empty(sk, w.D, dtype=w.dtype, device=dev)
     idx = torch.empty(sk, dtype=torch.int32, device=dev)
     src = torch.empty(sk, dtype=torch.uint8, device=dev)
 
     def step():
-        r.reduce(w.X, w.Xpre, w.Xpost, w.N, w.K, out=out, out_idx=idx, out_src=src)
+        r.reduce(w.X, *states, w.N, w.K, out=out, out_idx=idx, out_src=src)
 
     for _ in range(args.warmup):
         step()
@@ -145,16 +162,16 @@ def main():
     # Roofline of the dominant kernel: K launches of the scoring kernel (the
     # same kernel, launch configuration and inputs as inside a step) between
     # two HIP events recorded on the stream the library launches on.
-    key_imp = torch.empty(sum(w.N), dtype=torch.float32, device=dev)
-    key_s = torch.empty_like(key_imp)
+    key_imp = torch.empty(sum(w.N), dtype=torch.float32, device=dev) if need_x else None
+    key_s = torch.empty(sum(w.N), dtype=torch.float32, device=dev) if need_s else None
     stream = torch.cuda.current_stream(dev)
     for _ in range(3):
-        r.score(w.X, w.Xpre, w.Xpost, out=(key_imp, key_s))
+        r.score(xs, *states, out=(key_imp, key_s))
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     ev0.record(stream)
     for _ in range(args.steps):
-        r.score(w.X, w.Xpre, w.Xpost, out=(key_imp, key_s))
+        r.score(xs, *states, out=(key_imp, key_s))
     ev1.record(stream)
     torch.cuda.synchronize()
     score_ms = ev0.elapsed_time(ev1) / args.steps
@@ -172,13 +189,16 @@ def main():
     images_s = w.B * args.steps / elapsed
     rows = sum(w.N)
     e = w.X.element_size()
-    score_bytes = rows * (w.D + 2 * w.Dc) * e + rows * 8          # read X, X', X''; write 2 keys
+    # read X (if scored), X' and X'' (if s is scored); write one key per score
+    score_bytes = rows * (need_x * (w.D * e + 4) + need_s * (2 * w.Dc * e + 4))
     achieved = score_bytes / (score_ms * 1e-3) / 1e9
-    path_bytes = w.algorithmic_bytes()
-    traffic = measured_traffic()
+    path_bytes = w.algorithmic_bytes(score_x=need_x, score_states=need_s)
+    traffic = measured_traffic() if headline else None
 
     line = {
-        "metric": METRIC if args.workload == "llava" else "images/s (%s workload)" % args.workload,
+        "metric": METRIC if headline else "images/s (%s workload%s%s)" % (
+            args.workload, "" if w.lam == synth.LAMBDA else ", lambda=%g" % w.lam,
+            ", real-interval stride" if args.stride_real else ""),
         "value": round(images_s, 1),
         "unit": "images/s",
         "n_gpus": 1,
@@ -192,7 +212,9 @@ def main():
         "data": "synthetic",
         "config": {"workload": describe(w),
                    "images": w.B, "tokens": rows, "D": w.D, "Dc": w.Dc, "kept": sum(w.K),
-                   "lambda": round(w.lam, 6)},
+                   "lambda": round(w.lam, 6),
+                   "stride": "real-interval" if args.stride_real else "algorithm-1",
+                   "scores": "+".join(n for n, f in (("H2", need_x), ("s", need_s)) if f)},
         "tokens_per_s": round(rows * args.steps / elapsed, 1),
         "path_hbm": {"algorithmic_bytes": path_bytes,
                      "achieved_GBs": round(path_bytes / (ms_step * 1e-3) / 1e9, 1),

@@ -70,6 +70,15 @@ typedef enum {
     TR_BF16 = 1           /* bfloat16 elements (upper half of a binary32)     */
 } tr_dtype;
 
+/* Variants of the method, OR-ed into tr_params.flags (0 = Algorithm 1). */
+typedef enum {
+    /* Step 6 with the real-valued interval R / K2 (R = N - K1) that the
+     * method's prose states (Sec. "Methodology", diversity stage) instead of
+     * Algorithm 1's integer stride: X^div = sorted positions floor(j R / K2),
+     * j = 0 .. K2-1, which spreads the picks over the whole of X^rem. */
+    TR_FLAG_STRIDE_REAL = 1
+} tr_flag;
+
 /* Problem statement and capacities, fixed for the life of a context. */
 typedef struct {
     int32_t D;            /* elements per row of X and out (> 0)                   */
@@ -78,7 +87,7 @@ typedef struct {
     int32_t max_images;   /* largest B accepted by tr_reduce / tr_select (>= 1)     */
     int64_t max_tokens;   /* largest sum of N[b] accepted (>= 1, < 2^31)            */
     int32_t max_N;        /* largest single N[b] accepted (>= 1)                    */
-    int32_t reserved;     /* must be 0                                              */
+    int32_t flags;        /* OR of tr_flag values; 0 = the method as Algorithm 1 states */
     double lambda;        /* balance factor in [0, 1] (Algorithm 1; the paper's
                              efficiency setting is 1/3: 64 + 128 of 192)            */
     double keep_ratio;    /* used when K == NULL: K_b = clamp(floor(keep_ratio N_b),
@@ -94,8 +103,8 @@ tr_status tr_create(const tr_params* p, tr_ctx** out);
 
 /* The whole module (steps 1-7 above) on a packed batch of B images.
  *   X      device [sum N, D]   tokens scored by Eq. (3)-(4) and gathered
- *   X_pre  device [sum N, Dc]  pre-MLP states x'  (Eq. 5-6)
- *   X_post device [sum N, Dc]  post-MLP states x'' (Eq. 5-6)
+ *   X_pre  device [sum N, Dc]  pre-MLP states x'  (Eq. 5-6), or NULL (below)
+ *   X_post device [sum N, Dc]  post-MLP states x'' (Eq. 5-6), or NULL (below)
  *   B      number of images, 0 <= B <= max_images (B = 0 is a no-op)
  *   N      host [B], 1 <= N[b] <= max_N, sum N <= max_tokens
  *   K      host [B] with 1 <= K[b] <= N[b], or NULL to use keep_ratio
@@ -108,7 +117,14 @@ tr_status tr_create(const tr_params* p, tr_ctx** out);
  *   stream hipStream_t or NULL
  * X, X_pre, X_post and out may have any alignment (16-byte aligned bases and
  * row pitches take the vector path; others a scalar path with bit-identical
- * results). */
+ * results).
+ * A score that decides nothing is not computed and its inputs are not read:
+ * H2 when every image has K1 = 0 or K1 = N (lambda = 0, the paper's ablation
+ * without the importance stage) and out_h2 is NULL; s when every image has
+ * K2 = 0 or K2 = N - K1 (lambda = 1, the ablation without the diversity
+ * stage) and out_s is NULL.  In the latter case X_pre and X_post may be NULL
+ * (and are ignored if given); otherwise NULL gives TR_EINVAL.  The kept set
+ * is the same as with both scores computed. */
 tr_status tr_reduce(tr_ctx* ctx, const void* X, const void* X_pre,
                     const void* X_post, int32_t B, const int32_t* N,
                     const int32_t* K, void* out, int32_t* out_idx,
@@ -122,6 +138,9 @@ tr_status tr_reduce(tr_ctx* ctx, const void* X, const void* X_pre,
  *           row; ascending CV^2 is descending H2
  *   key_s   device float [rows]: s (Eq. 6)
  *   out_h2  device float [rows] or NULL: H2 = log D - log1p(CV^2)
+ * Either score may be left out: X, key_imp (and out_h2) all NULL computes s
+ * alone; X_pre, X_post and key_s all NULL computes the Stage I key alone.
+ * A partly given group, or nothing to compute, is TR_EINVAL.
  * rows may be any value >= 0 (no capacity applies). */
 tr_status tr_score(tr_ctx* ctx, const void* X, const void* X_pre,
                    const void* X_post, int64_t rows, float* key_imp,

@@ -51,11 +51,11 @@ def _ptr(t: Optional[torch.Tensor]):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
 
 
-def _params(D, Dc, dtype, lam, keep_ratio, max_images, max_tokens, max_N) -> Params:
+def _params(D, Dc, dtype, lam, keep_ratio, max_images, max_tokens, max_N, flags=0) -> Params:
     if dtype not in _DTYPES:
         raise TypeError("dtype must be torch.float32 or torch.bfloat16")
     return Params(D=int(D), Dc=int(Dc or 0), dtype=_DTYPES[dtype], max_images=int(max_images),
-                  max_tokens=int(max_tokens), max_N=int(max_N), reserved=0, lam=float(lam),
+                  max_tokens=int(max_tokens), max_N=int(max_N), flags=int(flags), lam=float(lam),
                   keep_ratio=float(keep_ratio or 0.0))
 
 
@@ -85,12 +85,16 @@ class ReduceResult(NamedTuple):
 
 
 class Reducer:
-    """A library context bound to one device, row widths, dtype and lambda."""
+    """A library context bound to one device, row widths, dtype and lambda.
+
+    stride_real selects the real-interval variant of the diversity stride
+    (positions floor(j R / K2) of the sorted remainder instead of j t).
+    """
 
     def __init__(self, D: int, Dc: Optional[int] = None, dtype: torch.dtype = torch.bfloat16,
                  lam: float = LAMBDA_PAPER, keep_ratio: Optional[float] = None,
                  max_images: int = 256, max_tokens: int = 1 << 20, max_N: Optional[int] = None,
-                 device=None):
+                 device=None, stride_real: bool = False):
         if not torch.cuda.is_available():
             raise RuntimeError("paper_2607_13500_amd needs a ROCm GPU (gfx950)")
         self.device = torch.device("cuda", torch.cuda.current_device() if device is None
@@ -101,7 +105,9 @@ class Reducer:
         if max_N is None:
             max_N = min(capacity_N_on(self.device), int(max_tokens))
         self.max_images, self.max_tokens, self.max_N = int(max_images), int(max_tokens), int(max_N)
-        p = _params(D, Dc, dtype, lam, keep_ratio, max_images, max_tokens, max_N)
+        self.stride_real = bool(stride_real)
+        p = _params(D, Dc, dtype, lam, keep_ratio, max_images, max_tokens, max_N,
+                    _lib.TR_FLAG_STRIDE_REAL if stride_real else 0)
         ctx = ctypes.c_void_p()
         with torch.cuda.device(self.device):
             _check(self.lib.tr_create(ctypes.byref(p), ctypes.byref(ctx)), "tr_create")
@@ -126,18 +132,28 @@ class Reducer:
         return Kb
 
     # -- the module ---------------------------------------------------------
-    def reduce(self, X: torch.Tensor, Xpre: torch.Tensor, Xpost: torch.Tensor,
+    def reduce(self, X: torch.Tensor, Xpre: Optional[torch.Tensor], Xpost: Optional[torch.Tensor],
                N: Sequence[int], K: Optional[Sequence[int]] = None, *,
                out: Optional[torch.Tensor] = None, out_idx: Optional[torch.Tensor] = None,
                out_src: Optional[torch.Tensor] = None, want_src: bool = True,
                want_scores: bool = False, stream=None) -> ReduceResult:
-        """Run score -> select -> gather on a packed batch (asynchronous)."""
+        """Run score -> select -> gather on a packed batch (asynchronous).
+
+        Xpre and Xpost may be None when no image's Stage II ranks tokens
+        (lambda = 1) and want_scores is False; the library then never reads
+        them.  Likewise H2 is not computed when no Stage I ranks (lambda = 0).
+        """
         self._check_rows("X", X, self.D)
-        self._check_rows("Xpre", Xpre, self.Dc)
-        self._check_rows("Xpost", Xpost, self.Dc)
+        if (Xpre is None) != (Xpost is None):
+            raise ValueError("Xpre and Xpost must both be given or both be None")
         rows = X.shape[0]
-        if Xpre.shape[0] != rows or Xpost.shape[0] != rows or sum(int(n) for n in N) != rows:
-            raise ValueError("X, Xpre, Xpost must have sum(N) = %d rows" % sum(int(n) for n in N))
+        if Xpre is not None:
+            self._check_rows("Xpre", Xpre, self.Dc)
+            self._check_rows("Xpost", Xpost, self.Dc)
+            if Xpre.shape[0] != rows or Xpost.shape[0] != rows:
+                raise ValueError("X, Xpre, Xpost must have the same number of rows")
+        if sum(int(n) for n in N) != rows:
+            raise ValueError("X must have sum(N) = %d rows" % sum(int(n) for n in N))
         sk = sum(self.kept_counts(N, K)) if len(N) else 0
         dev = self.device
         if out is None:
@@ -161,28 +177,40 @@ class Reducer:
         _check(st, "tr_reduce")
         return ReduceResult(out, out_idx, out_src, h2, s)
 
-    def score(self, X: torch.Tensor, Xpre: torch.Tensor, Xpost: torch.Tensor, *,
-              want_h2: bool = False, out=None, stream=None):
-        """Scoring kernel alone: (CV^2 key, s, H2 or None), float32 [rows] each.
+    def score(self, X: Optional[torch.Tensor], Xpre: Optional[torch.Tensor],
+              Xpost: Optional[torch.Tensor], *, want_h2: bool = False, out=None, stream=None):
+        """Scoring kernel alone: (CV^2 key, s, H2), float32 [rows] each.
 
-        ``out`` may pass preallocated (CV^2, s) tensors.
+        X = None skips the Stage I key (CV^2 and H2 come back None); Xpre =
+        Xpost = None skips s.  ``out`` may pass preallocated (CV^2, s)
+        tensors (None for a skipped one).
         """
-        self._check_rows("X", X, self.D)
-        self._check_rows("Xpre", Xpre, self.Dc)
-        self._check_rows("Xpost", Xpost, self.Dc)
-        rows = X.shape[0]
-        if Xpre.shape[0] != rows or Xpost.shape[0] != rows:
-            raise ValueError("X, Xpre and Xpost must have the same number of rows")
+        if X is None and Xpre is None:
+            raise ValueError("nothing to score")
+        if (Xpre is None) != (Xpost is None):
+            raise ValueError("Xpre and Xpost must both be given or both be None")
+        rows = None
+        for name, t, width in (("X", X, self.D), ("Xpre", Xpre, self.Dc), ("Xpost", Xpost, self.Dc)):
+            if t is None:
+                continue
+            self._check_rows(name, t, width)
+            if rows is None:
+                rows = t.shape[0]
+            elif t.shape[0] != rows:
+                raise ValueError("X, Xpre and Xpost must have the same number of rows")
         f32 = dict(dtype=torch.float32, device=self.device)
         if out is not None:
             cv2, s = out
-            for t in (cv2, s):
-                if t.dtype != torch.float32 or t.device != self.device or t.dim() != 1 \
-                        or t.numel() != rows or not t.is_contiguous():
-                    raise ValueError("score outputs must be contiguous float32 [rows] tensors")
         else:
-            cv2, s = torch.empty(rows, **f32), torch.empty(rows, **f32)
-        h2 = torch.empty(rows, **f32) if want_h2 else None
+            cv2 = torch.empty(rows, **f32) if X is not None else None
+            s = torch.empty(rows, **f32) if Xpre is not None else None
+        for t, given in ((cv2, X), (s, Xpre)):
+            if (t is None) != (given is None):
+                raise ValueError("score outputs must match the inputs given")
+            if t is not None and (t.dtype != torch.float32 or t.device != self.device or t.dim() != 1
+                                  or t.numel() != rows or not t.is_contiguous()):
+                raise ValueError("score outputs must be contiguous float32 [rows] tensors")
+        h2 = torch.empty(rows, **f32) if want_h2 and X is not None else None
         st = self.lib.tr_score(self._ctx, _ptr(X), _ptr(Xpre), _ptr(Xpost), rows, _ptr(cv2),
                                _ptr(s), _ptr(h2), self._stream(stream))
         _check(st, "tr_score")

@@ -25,7 +25,7 @@ class Params(ctypes.Structure):
         ("max_images", ctypes.c_int32),
         ("max_tokens", ctypes.c_int64),
         ("max_N", ctypes.c_int32),
-        ("reserved", ctypes.c_int32),
+        ("flags", ctypes.c_int32),
         ("lam", ctypes.c_double),
         ("keep_ratio", ctypes.c_double),
     ]
@@ -33,6 +33,7 @@ class Params(ctypes.Structure):
 
 TR_OK, TR_EINVAL, TR_ENOMEM, TR_EUNSUPPORTED, TR_EDEVICE = range(5)
 TR_FP32, TR_BF16 = 0, 1
+TR_FLAG_STRIDE_REAL = 1
 
 _lib = None
 

@@ -47,7 +47,7 @@ tr_status check_params(const tr_params* p, bool need_caps)
     if (p->Dc < 0) return fail(TR_EINVAL, "Dc must be >= 0 (got %d)", p->Dc);
     if (p->dtype != TR_FP32 && p->dtype != TR_BF16)
         return fail(TR_EINVAL, "dtype must be TR_FP32 or TR_BF16 (got %d)", p->dtype);
-    if (p->reserved != 0) return fail(TR_EINVAL, "reserved field must be 0");
+    if (p->flags & ~(int32_t)TR_FLAG_STRIDE_REAL) return fail(TR_EINVAL, "unknown flags 0x%x", p->flags);
     if (!(p->lambda >= 0.0 && p->lambda <= 1.0))
         return fail(TR_EINVAL, "lambda must be in [0, 1] (got %g)", p->lambda);
     if (!(p->keep_ratio == 0.0 || (p->keep_ratio > 0.0 && p->keep_ratio <= 1.0)))
@@ -71,6 +71,8 @@ struct Plan {
     int64_t sum_k = 0;
     int nmax = 0;
     bool uniform = true;
+    bool keys_imp = false;   // some image's Stage I depends on the key order (0 < K1 < N)
+    bool keys_s = false;     // some image's Stage II does (0 < K2 < N - K1)
 };
 
 // Algorithm 1, step 1 (K1 = floor(lambda K) in double, K2 = K - K1) and the
@@ -113,6 +115,8 @@ tr_status make_plan(const tr_params* p, int32_t B, const int32_t* N, const int32
         d.k2 = k2;
         d.t = t;
         d.out_off = (int32_t)outs;
+        if (k1 > 0 && k1 < n) out.keys_imp = true;
+        if (k2 > 0 && k2 < n - k1) out.keys_s = true;
         rows += n;
         outs += k;
         if (rows > (int64_t)INT32_MAX) return fail(TR_EINVAL, "sum of N exceeds 2^31 - 1");
@@ -202,6 +206,7 @@ hipError_t run_select(const tr_ctx* c, const Plan& pl, const float* key_imp, con
     a.out_rows = out_rows;
     a.gsel = c->gsel;
     a.gimp = c->gimp;
+    a.stride_real = (c->p.flags & TR_FLAG_STRIDE_REAL) ? 1 : 0;
     const int B = (int)pl.desc.size();
     if (B == 0) return hipSuccess;
     if (pl.uniform) {
@@ -315,8 +320,12 @@ tr_status tr_create(const tr_params* p, tr_ctx** out)
         tr_destroy(c);
         return fail(TR_ENOMEM, "hipMalloc of %zu-token scratch failed: %s", n, hipGetErrorString(e));
     }
-    // The split selection leaves the pick bitmaps zero after every call.
+    // The split selection leaves the pick bitmaps zero after every call.  The
+    // key scratch starts at zero so that a call that needs neither key (every
+    // image keeps all its tokens of a stage) selects from defined values.
     if ((e = hipMemset(c->gsel, 0, gw * sizeof(uint32_t))) != hipSuccess ||
+        (e = hipMemset(c->key_imp, 0, n * sizeof(float))) != hipSuccess ||
+        (e = hipMemset(c->key_s, 0, n * sizeof(float))) != hipSuccess ||
         (e = hipDeviceSynchronize()) != hipSuccess) {
         tr_destroy(c);
         return hip_fail(e, "scratch initialisation");
@@ -396,8 +405,16 @@ tr_status tr_reduce(tr_ctx* c, const void* X, const void* X_pre, const void* X_p
     tr_status st = check_ctx_plan(c, B, N, K, pl);
     if (st != TR_OK) return st;
     if (B == 0) return TR_OK;
-    if (!X || !X_pre || !X_post || !out || !out_idx)
-        return fail(TR_EINVAL, "X, X_pre, X_post, out and out_idx must be non-NULL");
+    if (!X || !out || !out_idx) return fail(TR_EINVAL, "X, out and out_idx must be non-NULL");
+    // Which scores the call needs: Stage I's when some image ranks by it or
+    // H2 is asked for, Stage II's likewise (lambda = 1 never needs s, lambda
+    // = 0 never needs H2).  A score that is not needed is not computed and its
+    // inputs are not read.
+    const int mode = (pl.keys_imp || out_h2 ? tr::kScoreImp : 0) | (pl.keys_s || out_s ? tr::kScoreSim : 0);
+    const bool need_c = (mode & tr::kScoreSim) != 0;
+    if (need_c && (!X_pre || !X_post))
+        return fail(TR_EINVAL, "X_pre and X_post must be non-NULL when Stage II ranks tokens or out_s is set");
+    if (!need_c) X_pre = X_post = nullptr;
     const uintptr_t em = (uintptr_t)c->eb - 1;
     if (((uintptr_t)X | (uintptr_t)X_pre | (uintptr_t)X_post | (uintptr_t)out) & em)
         return fail(TR_EINVAL, "tensor base pointers must be aligned to the element size");
@@ -421,20 +438,22 @@ tr_status tr_reduce(tr_ctx* c, const void* X, const void* X_pre, const void* X_p
     hipError_t e;
     if (ev && (e = hipEventRecord(ev[0], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
 
-    tr::ScoreArgs sa;
-    sa.X = X;
-    sa.P = X_pre;
-    sa.Q = X_post;
-    sa.rows = pl.sum_n;
-    sa.D = c->p.D;
-    sa.Dc = c->Dc;
-    sa.key_imp = c->key_imp;
-    sa.key_s = c->key_s;
-    sa.out_h2 = out_h2;
-    sa.out_s = out_s;
-    sa.logD = (float)log((double)c->p.D);
-    if ((e = tr::launch_score(sa, c->p.dtype == TR_BF16, vec_score, s)) != hipSuccess)
-        return hip_fail(e, "score kernel launch");
+    if (mode) {
+        tr::ScoreArgs sa;
+        sa.X = X;
+        sa.P = X_pre;
+        sa.Q = X_post;
+        sa.rows = pl.sum_n;
+        sa.D = c->p.D;
+        sa.Dc = c->Dc;
+        sa.key_imp = c->key_imp;
+        sa.key_s = c->key_s;
+        sa.out_h2 = out_h2;
+        sa.out_s = out_s;
+        sa.logD = (float)log((double)c->p.D);
+        if ((e = tr::launch_score(sa, c->p.dtype == TR_BF16, vec_score, mode, s)) != hipSuccess)
+            return hip_fail(e, "score kernel launch");
+    }
     if (ev && (e = hipEventRecord(ev[1], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
 
     if ((e = run_select(c, pl, c->key_imp, c->key_s, out_idx, out_src, c->rows, s)) != hipSuccess)
@@ -454,8 +473,12 @@ tr_status tr_score(tr_ctx* c, const void* X, const void* X_pre, const void* X_po
     if (!c) return fail(TR_EINVAL, "ctx is NULL");
     if (rows < 0) return fail(TR_EINVAL, "rows must be >= 0");
     if (rows == 0) return TR_OK;
-    if (!X || !X_pre || !X_post || !key_imp || !key_s)
-        return fail(TR_EINVAL, "X, X_pre, X_post, key_imp and key_s must be non-NULL");
+    const bool want_x = X || key_imp || out_h2;
+    const bool want_c = X_pre || X_post || key_s;
+    if (!want_x && !want_c) return fail(TR_EINVAL, "nothing to compute: every tensor is NULL");
+    if (want_x && (!X || !key_imp)) return fail(TR_EINVAL, "X and key_imp go together (out_h2 needs both)");
+    if (want_c && (!X_pre || !X_post || !key_s))
+        return fail(TR_EINVAL, "X_pre, X_post and key_s go together");
     const uintptr_t em = (uintptr_t)c->eb - 1;
     if (((uintptr_t)X | (uintptr_t)X_pre | (uintptr_t)X_post) & em)
         return fail(TR_EINVAL, "tensor base pointers must be aligned to the element size");
@@ -479,7 +502,8 @@ tr_status tr_score(tr_ctx* c, const void* X, const void* X_pre, const void* X_po
     sa.out_h2 = out_h2;
     sa.out_s = nullptr;
     sa.logD = (float)log((double)c->p.D);
-    hipError_t e = tr::launch_score(sa, c->p.dtype == TR_BF16, vec, static_cast<hipStream_t>(stream));
+    const int mode = (want_x ? tr::kScoreImp : 0) | (want_c ? tr::kScoreSim : 0);
+    hipError_t e = tr::launch_score(sa, c->p.dtype == TR_BF16, vec, mode, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "score kernel launch");
     return TR_OK;
 }

@@ -18,17 +18,23 @@ struct ScoreArgs {
     int64_t rows;
     int32_t D;
     int32_t Dc;
-    float* key_imp;      // [rows] CV^2 of |x| (Stage I key, ascending)
-    float* key_s;        // [rows] s (Stage II key, ascending)
+    float* key_imp;      // [rows] CV^2 of |x| (Stage I key, ascending), or nullptr
+    float* key_s;        // [rows] s (Stage II key, ascending), or nullptr
     float* out_h2;       // [rows] or nullptr
     float* out_s;        // [rows] or nullptr
     float logD;          // log(D) in fp32
 };
 
+// Which scores a launch computes (a bit set, never 0).  A score left out
+// reads nothing: its key (if the pointer is set) is written as 0, and its
+// optional output is not written.
+constexpr int kScoreImp = 1;   // Eq. (3)-(4) from X: key_imp, out_h2
+constexpr int kScoreSim = 2;   // Eq. (6) from X_pre, X_post: key_s, out_s
+
 // bf16: true for bfloat16 rows, false for fp32.  vec: every row start is
 // 16-byte aligned (vector loads); otherwise element loads with the same
 // per-lane arithmetic order.
-hipError_t launch_score(const ScoreArgs& a, bool bf16, bool vec, hipStream_t s);
+hipError_t launch_score(const ScoreArgs& a, bool bf16, bool vec, int mode, hipStream_t s);
 
 // ---- per-image selection (top-K1, ordered remainder, sort, stride) --------
 struct ImageDesc {
@@ -54,6 +60,7 @@ struct SelectArgs {
     int32_t nimg;           // images in this launch
     int32_t img0;           // index of the first image of this launch in the batch
     int32_t groups;         // workgroups per image (1, or more to split large images)
+    int32_t stride_real;    // 1: X^div at floor(j R / K2) instead of j t
     ImageDesc desc[kMaxDescPerLaunch];
 };
 

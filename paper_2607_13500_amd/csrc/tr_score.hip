@@ -21,6 +21,11 @@
 //
 // Lane partial sums are combined by a fixed DPP scan tree (the total is read
 // from lane 63 into every lane) and lane 0 writes the results.
+//
+// A launch may compute only one of the two scores (Stage I's key alone, or
+// Stage II's alone): the other tensor is then never read and its key is
+// written as 0.  The scores that are computed are bit-identical to those of a
+// launch that computes both, because each score's arithmetic is independent.
 #include "tr_internal.h"
 #include "tr_wave.h"
 
@@ -173,11 +178,13 @@ __device__ __forceinline__ float abs_sum(const float* v, int m)
     return s;
 }
 
-template <bool BF16, bool VEC, int UNR>
+template <bool BF16, bool VEC, int UNR, int MODE>
 __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a)
 {
     using L = Layout<BF16>;
     constexpr int V = L::kV;
+    constexpr bool kX = (MODE & kScoreImp) != 0;    // Eq. (3)-(4) over X
+    constexpr bool kC = (MODE & kScoreSim) != 0;    // Eq. (6) over X_pre, X_post
     const int lane = threadIdx.x & (kWave - 1);
     const int64_t row = (int64_t)blockIdx.x * (blockDim.x / kWave) + (threadIdx.x / kWave);
     if (row >= a.rows) return;   // whole wavefront leaves together
@@ -185,15 +192,15 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a)
     const char* xr = static_cast<const char*>(a.X) + row * (int64_t)a.D * L::kEB;
     const char* pr = static_cast<const char*>(a.P) + row * (int64_t)a.Dc * L::kEB;
     const char* qr = static_cast<const char*>(a.Q) + row * (int64_t)a.Dc * L::kEB;
-    const int nfx = a.D / V;    // full chunks of X
-    const int nfc = a.Dc / V;   // full chunks of X_pre / X_post
+    const int nfx = kX ? a.D / V : 0;    // full chunks of X
+    const int nfc = kC ? a.Dc / V : 0;   // full chunks of X_pre / X_post
     const int nf = nfx > nfc ? nfx : nfc;
     // elements in the lanes' first chunks: the sample the shift c averages
     const float n_probe = (float)(a.D < kWave * V ? a.D : kWave * V);
 
     // A trailing partial chunk belongs to lane (index % 64) like any other and
     // is that lane's last chunk.
-    const bool tail_x = (a.D % V) && (nfx & (kWave - 1)) == lane;
+    const bool tail_x = kX && (a.D % V) && (nfx & (kWave - 1)) == lane;
     const int mx = a.D - nfx * V;
     float tx[V];
     if (tail_x) load_partial<BF16>(xr, nfx, mx, tx);
@@ -201,7 +208,7 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a)
     XAcc xa{0.f, 0.f};
     CAcc ca{0.f, 0.f, 0.f};
     float c = 0.f;
-    if (nfx == 0) c = wave_sum(tail_x ? abs_sum<V>(tx, mx) : 0.f) / n_probe;
+    if (kX && nfx == 0) c = wave_sum(tail_x ? abs_sum<V>(tx, mx) : 0.f) / n_probe;
 
     for (int j0 = 0; j0 < nf; j0 += kWave * UNR) {   // same trip count for every lane
         Raw rx[UNR], rp[UNR], rq[UNR];
@@ -237,58 +244,78 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a)
         }
     }
     if (tail_x) x_chunk(xa, tx, mx, c);
-    if (a.Dc % V && (nfc & (kWave - 1)) == lane) {
+    if (kC && a.Dc % V && (nfc & (kWave - 1)) == lane) {
         const int m = a.Dc - nfc * V;
         c_chunk<BF16>(ca, load_partial_raw<BF16>(pr, nfc, m), load_partial_raw<BF16>(qr, nfc, m));
     }
 
-    const float sd = wave_sum(xa.sd);
-    const float sd2 = wave_sum(xa.sd2);
-    const float dot = wave_sum(ca.dot);
-    const float n1 = wave_sum(ca.n1);
-    const float n2 = wave_sum(ca.n2);
+    float sd = 0.f, sd2 = 0.f, dot = 0.f, n1 = 0.f, n2 = 0.f;
+    if constexpr (kX) {
+        sd = wave_sum(xa.sd);
+        sd2 = wave_sum(xa.sd2);
+    }
+    if constexpr (kC) {
+        dot = wave_sum(ca.dot);
+        n1 = wave_sum(ca.n1);
+        n2 = wave_sum(ca.n2);
+    }
 
     if (lane == 0) {
-        const float Df = (float)a.D;
-        const float mean = c + sd / Df;
-        const float m2 = fmaxf(0.f, fmaf(-sd, sd / Df, sd2));
-        float cv2, h2;
-        if (mean > 0.f) {
-            cv2 = (m2 / (mean * Df)) / mean;
-            h2 = a.logD - log1pf(cv2);
-        } else {   // all-zero row: H2 = 0, i.e. 1 + CV^2 = D
-            cv2 = Df - 1.f;
-            h2 = 0.f;
+        float cv2 = 0.f, h2 = 0.f;
+        if constexpr (kX) {
+            const float Df = (float)a.D;
+            const float mean = c + sd / Df;
+            const float m2 = fmaxf(0.f, fmaf(-sd, sd / Df, sd2));
+            if (mean > 0.f) {
+                cv2 = (m2 / (mean * Df)) / mean;
+                h2 = a.logD - log1pf(cv2);
+            } else {   // all-zero row: H2 = 0, i.e. 1 + CV^2 = D
+                cv2 = Df - 1.f;
+                h2 = 0.f;
+            }
         }
         float s = 0.f;
-        if (n1 > 0.f && n2 > 0.f) s = dot / (sqrtf(n1) * sqrtf(n2));
-        a.key_imp[row] = cv2;
-        a.key_s[row] = s;
-        if (a.out_h2) a.out_h2[row] = h2;
-        if (a.out_s) a.out_s[row] = s;
+        if constexpr (kC) {
+            if (n1 > 0.f && n2 > 0.f) s = dot / (sqrtf(n1) * sqrtf(n2));
+        }
+        if (a.key_imp) a.key_imp[row] = cv2;
+        if (a.key_s) a.key_s[row] = s;
+        if (kX && a.out_h2) a.out_h2[row] = h2;
+        if (kC && a.out_s) a.out_s[row] = s;
     }
 }
 
 // One wavefront per workgroup: the finest scheduling grain spreads rows evenly
 // over the 256 CUs (measured 128 us vs 136 us with four-wavefront groups on
 // 64 x 576 x 4096 bf16 rows, the latter equal to a plain read of the bytes).
-template <bool BF16, bool VEC>
+template <bool BF16, bool VEC, int MODE>
 hipError_t launch_t(const ScoreArgs& a, hipStream_t s)
 {
     constexpr int kThreads = 64;
     constexpr int kRowsPerBlock = kThreads / kWave;
     const int64_t blocks = (a.rows + kRowsPerBlock - 1) / kRowsPerBlock;
     if (blocks <= 0) return hipSuccess;
-    hipLaunchKernelGGL((score_kernel<BF16, VEC, 4>), dim3((unsigned)blocks), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL((score_kernel<BF16, VEC, 4, MODE>), dim3((unsigned)blocks), dim3(kThreads), 0, s, a);
     return hipGetLastError();
+}
+
+template <bool BF16, bool VEC>
+hipError_t launch_m(const ScoreArgs& a, int mode, hipStream_t s)
+{
+    switch (mode) {
+    case kScoreImp: return launch_t<BF16, VEC, kScoreImp>(a, s);
+    case kScoreSim: return launch_t<BF16, VEC, kScoreSim>(a, s);
+    default: return launch_t<BF16, VEC, kScoreImp | kScoreSim>(a, s);
+    }
 }
 
 }  // namespace
 
-hipError_t launch_score(const ScoreArgs& a, bool bf16, bool vec, hipStream_t s)
+hipError_t launch_score(const ScoreArgs& a, bool bf16, bool vec, int mode, hipStream_t s)
 {
-    if (bf16) return vec ? launch_t<true, true>(a, s) : launch_t<true, false>(a, s);
-    return vec ? launch_t<false, true>(a, s) : launch_t<false, false>(a, s);
+    if (mode != kScoreImp && mode != kScoreSim && mode != (kScoreImp | kScoreSim)) return hipErrorInvalidValue;
+    if (bf16) return vec ? launch_m<true, true>(a, mode, s) : launch_m<true, false>(a, mode, s);
+    return vec ? launch_m<false, true>(a, mode, s) : launch_m<false, false>(a, mode, s);
 }
 
 }  // namespace tr

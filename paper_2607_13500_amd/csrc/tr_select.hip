@@ -4,7 +4,8 @@
 // Keys are fp32 scores mapped to order-preserving u32 (-0 == +0).  Stage I
 // keeps the K1 smallest Stage I keys (ties: lower index); Stage II orders
 // X^rem by the Stage II key (ties: lower index) and keeps sorted positions
-// 0, t, ..., (K2-1) t; the output lists X^imp U X^div in token order.
+// 0, t, ..., (K2-1) t (or floor(j R / K2) in the real-interval variant); the
+// output lists X^imp U X^div in token order.
 //
 // Stage I narrows a bucket {k : (k & pmask) == prefix} that contains the K1-th
 // smallest key with 8-bit digit passes over the highest still-undecided bits
@@ -450,20 +451,37 @@ __device__ void stage1_mark_counted(const uint32_t* ki, int N, uint32_t prefix, 
 // order (n u16).  H (B words) must be zero.  Returns false, having written
 // only H, cur, list and slot rows, when a bucket holds more than kBucketLimit
 // tokens or the key range is not finite.
+// X^div positions in the ascending order of X^rem (R tokens, K2 picks).
+// Algorithm 1: 0, t, ..., (K2 - 1) t.  Real-interval variant (the interval
+// R / K2 of the method's prose): floor(j R / K2), j < K2.  Every product
+// stays below 2^32 because R, K2 <= 65535.
+struct Stride {
+    uint32_t t, R, K2;
+    bool real;
+    // Is rank r a pick?  Real variant: the smallest j with floor(j R / K2) >=
+    // r is ceil(r K2 / R); r is a pick iff that j is in range and lands on r.
+    __device__ __forceinline__ bool picks(uint32_t r) const
+    {
+        if (!real) return r % t == 0 && r < K2 * t;
+        const uint32_t j = (r * K2 + R - 1) / R;
+        return j < K2 && (j * R) / K2 == r;
+    }
+    __device__ __forceinline__ uint32_t pos(uint32_t j) const { return real ? (j * R) / K2 : j * t; }
+};
+
 // Result of stage2_bucket.
 constexpr int kS2Failed = 0;   // nothing decided: sort instead
 constexpr int kS2Local = 1;    // every pick is in bsel
 constexpr int kS2Global = 2;   // this group's picks are in the global bitmap
 
 __device__ int stage2_bucket(const uint32_t* ks, const uint32_t* bimp, uint32_t* bsel, int N,
-                              int R, int K2, int t, uint32_t* H, uint32_t* cur, uint16_t* list,
+                              int R, const Stride& sp, uint32_t* H, uint32_t* cur, uint16_t* list,
                               uint32_t* row_lo, uint32_t* row_hi, uint32_t* row_a, uint32_t* row_b,
                               int part, int parts, uint32_t* gpick)
 {
     const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
     int beg, end;
     wave_range(N, w, beg, end);
-    const uint32_t span = (uint32_t)K2 * (uint32_t)t;
 
     // key range of X^rem (max of the complement gives the minimum)
     uint32_t nlo = 0, hi = 0;
@@ -501,7 +519,7 @@ __device__ int stage2_bucket(const uint32_t* ks, const uint32_t* bimp, uint32_t*
             const bool rem = i < end && !bit_of(bimp, i);
             const uint64_t br = __ballot(rem);
             const uint32_t r = r0 + (uint32_t)__popcll(br & lanes_below(lane));
-            const uint64_t bp = __ballot(rem && r % (uint32_t)t == 0 && r < span);
+            const uint64_t bp = __ballot(rem && sp.picks(r));
             if (lane == 0) bsel[base >> 5] = bimp[base >> 5] | (uint32_t)bp;
             if (lane == 32) bsel[(base >> 5) + 1] = bimp[(base >> 5) + 1] | (uint32_t)(bp >> 32);
             r0 += (uint32_t)__popcll(br);
@@ -583,7 +601,7 @@ __device__ int stage2_bucket(const uint32_t* ks, const uint32_t* bimp, uint32_t*
                     }
                 }
                 const uint32_t rr = start + r;
-                if (have && rr % (uint32_t)t == 0 && rr < span) {
+                if (have && sp.picks(rr)) {
                     if (gpick) atomicOr(&gpick[myid >> 5], 1u << (myid & 31));
                     else atomicOr(&bsel[myid >> 5], 1u << (myid & 31));
                 }
@@ -613,7 +631,7 @@ __device__ int stage2_bucket(const uint32_t* ks, const uint32_t* bimp, uint32_t*
                 const uint32_t ij = list[j], kj = ks[ij];
                 r += (kj < key || (kj == key && ij < (uint32_t)i)) ? 1u : 0u;
             }
-            picked = r % (uint32_t)t == 0 && r < span;
+            picked = sp.picks(r);
         }
         const uint64_t bp = __ballot(picked);
         if (lane == 0) bsel[base >> 5] = bimp[base >> 5] | (uint32_t)bp;
@@ -625,7 +643,7 @@ __device__ int stage2_bucket(const uint32_t* ks, const uint32_t* bimp, uint32_t*
 // Stage II by ordered compaction and a stable LSD radix sort of 16-bit
 // indices; sets the X^div bits in bsel.  idx_a / idx_b hold n u16 each.
 __device__ void stage2_radix(const uint32_t* ks, const uint32_t* bimp, uint32_t* bsel, int N, int K1,
-                             int K2, int t, uint32_t VS, uint16_t* idx_a, uint16_t* idx_b,
+                             const Stride& sp, uint32_t VS, uint16_t* idx_a, uint16_t* idx_b,
                              uint16_t* hist, uint32_t* row_c, uint32_t* row_s)
 {
     const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
@@ -693,8 +711,8 @@ __device__ void stage2_radix(const uint32_t* ks, const uint32_t* bimp, uint32_t*
         dst = tmp;
     }
     __syncthreads();   // the compaction (or the last pass) is visible to every picker
-    for (int j = tid; j < K2; j += kThreads) {
-        const int id = src[j * t];
+    for (int j = tid; j < (int)sp.K2; j += kThreads) {
+        const int id = src[sp.pos((uint32_t)j)];
         atomicOr(&bsel[id >> 5], 1u << (id & 31));
     }
 }
@@ -790,13 +808,14 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a)
         uint16_t* idx = reinterpret_cast<uint16_t*>(ki);
         const size_t wbase = (size_t)(d.row_off >> 5) + 2 * (size_t)img;
         uint32_t* gpick = split ? a.gsel + wbase : nullptr;
-        int st = stage2_bucket(ks, bimp, bsel, N, N - K1, K2, d.t, area, area + kBuckets, idx,
+        const Stride sp{(uint32_t)d.t, (uint32_t)(N - K1), (uint32_t)K2, a.stride_real != 0};
+        int st = stage2_bucket(ks, bimp, bsel, N, N - K1, sp, area, area + kBuckets, idx,
                                slots + 6 * kW, slots + 7 * kW, slots + 2 * kW, slots + 3 * kW,
                                split ? part : 0, split ? G : 1, gpick);
         if (st == kS2Failed) {
             if (part > 0) return;   // the same decision in every group: group 0 sorts
             __syncthreads();        // every thread is past the bucket attempt
-            stage2_radix(ks, bimp, bsel, N, K1, K2, d.t, VS, idx, idx + N,
+            stage2_radix(ks, bimp, bsel, N, K1, sp, VS, idx, idx + N,
                          reinterpret_cast<uint16_t*>(area), slots + 4 * kW, slots + 5 * kW);
             st = kS2Local;
         }

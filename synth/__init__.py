@@ -73,10 +73,13 @@ class Workload:
     def dtype(self) -> torch.dtype:
         return self.X.dtype
 
-    def algorithmic_bytes(self) -> int:
-        """Compulsory HBM bytes of one reduction: read X, Xpre, Xpost, write out."""
+    def algorithmic_bytes(self, score_x: bool = True, score_states: bool = True) -> int:
+        """Compulsory HBM bytes of one reduction: read X (every row when it is
+        scored, else only the kept rows), Xpre and Xpost (when s is scored),
+        write out."""
         e = self.X.element_size()
-        return sum(e * (n * self.D + 2 * n * self.Dc + k * self.D) for n, k in zip(self.N, self.K))
+        return sum(e * ((n if score_x else k) * self.D + (2 * n * self.Dc if score_states else 0)
+                        + k * self.D) for n, k in zip(self.N, self.K))
 
 
 def _gen(device, seed):

@@ -13,8 +13,9 @@ score gap is inside the window an fp32 score error of TOL can cross:
       each such token is a counted near-tie swap, anything else fails.
 * P3  Stage II, checked on the GPU's own X^imp so that a P2 swap cannot
       cascade: order X^rem by the oracle's (s, index); the GPU's j-th pick (in
-      its own s order) must be the token at sorted position j t, or a token
-      whose oracle s is within 2 TOL of it (a counted near tie).
+      its own s order) must be the token at sorted position j t (floor(j R /
+      K2) in the real-interval variant), or a token whose oracle s is within
+      2 TOL of it (a counted near tie).
 * P4  output: K kept, strictly ascending, K1 from Stage I and K2 from Stage II,
       and out equal byte for byte to the kept rows of X.
 * P5  information only: raw mismatch count against the oracle's indices.
@@ -58,38 +59,48 @@ class Report:
                    self.raw_mismatch, len(self.failures)))
 
 
-def oracle_reference(w, want_out=False):
+def oracle_reference(w, want_out=False, stride_mode=0):
     """Run the oracle on CPU copies of a workload (the same bytes the GPU sees)."""
     return oracle.reduce(w.X.cpu(), w.Xpre.cpu(), w.Xpost.cpu(), w.N, w.K, w.lam,
-                         want_out=want_out, want_scores=True)
+                         want_out=want_out, want_scores=True, stride_mode=stride_mode)
+
+
+def stride_positions(R: int, K2: int, t: int, stride_mode: int = 0) -> np.ndarray:
+    """Sorted positions of X^div: j t (Algorithm 1) or floor(j R / K2) (real interval)."""
+    j = np.arange(K2, dtype=np.int64)
+    return (j * R) // K2 if stride_mode == 1 else j * t
 
 
 def cv2_from_h2(h2: np.ndarray, D: int) -> np.ndarray:
     return np.expm1(math.log(D) - h2)
 
 
-def check(w, res, ref, cv2_gpu=None, tol: float = TOL) -> Report:
-    """Apply P1-P5 to a GPU ReduceResult (with scores) against an oracle run."""
+def check(w, res, ref, cv2_gpu=None, tol: float = TOL, stride_mode: int = 0) -> Report:
+    """Apply P1-P5 to a GPU ReduceResult against an oracle run.
+
+    res.h2 / res.s may be None (a run that did not return scores); P1 then
+    checks only what was given, and P3 orders the GPU picks by the oracle's s.
+    """
     rep = Report()
     D = w.D
     h2o, so = ref["h2"], ref["s"]
     cv2o = cv2_from_h2(h2o, D)
     rep.tokens = h2o.size
+    sg = None
     if res.h2 is not None:
         h2g = res.h2.double().cpu().numpy()
-        sg = res.s.double().cpu().numpy()
         dh = np.abs(h2g - h2o)
-        ds = np.abs(sg - so)
         rep.max_abs_h2 = float(dh.max(initial=0))
-        rep.max_abs_s = float(ds.max(initial=0))
         bad = np.nonzero(dh > tol * np.maximum(1.0, np.abs(h2o)))[0]
         if bad.size:
             rep.failures.append("P1 H2 outside tolerance at rows %s" % bad[:8].tolist())
+    if res.s is not None:
+        sg = res.s.double().cpu().numpy()
+        ds = np.abs(sg - so)
+        rep.max_abs_s = float(ds.max(initial=0))
         bad = np.nonzero(ds > tol * np.maximum(1.0, np.abs(so)))[0]
         if bad.size:
             rep.failures.append("P1 s outside tolerance at rows %s" % bad[:8].tolist())
-    else:
-        sg = None
     if cv2_gpu is not None:
         cg = cv2_gpu.double().cpu().numpy()
         dc = np.abs(cg - cv2o)
@@ -149,7 +160,7 @@ def check(w, res, ref, cv2_gpu=None, tol: float = TOL) -> Report:
             in_imp[imp_g] = True
             rem = np.nonzero(~in_imp)[0]
             order = rem[np.lexsort((rem, s_img[rem]))]
-            expect = order[np.arange(K2) * t]
+            expect = order[stride_positions(rem.size, K2, t, stride_mode)]
             div = idx[src == 1]
             if np.any(in_imp[div]):
                 rep.failures.append("P3 image %d: a Stage II pick is also in X^imp" % b)

@@ -161,12 +161,9 @@ def test_misaligned_pointers_give_identical_results():
     r.close()
 
 
-def test_select_bit_exact_on_given_keys():
-    """Integer work: with the same fp32 keys, the GPU selection equals the oracle's exactly."""
-    import paper_2607_13500_amd as tr
-    rng = np.random.default_rng(11)
+def _select_cases(rng, trials=60):
     cases = []
-    for trial in range(60):
+    for trial in range(trials):
         B = int(rng.integers(1, 7))
         N = [int(rng.choice([1, 2, 63, 64, 65, 200, 576, 1000, 2880, 4097, 9000]))
              for _ in range(B)]
@@ -182,41 +179,62 @@ def test_select_bit_exact_on_given_keys():
     for n in (100, 576, 3000, 4096, 5000):
         for shape in ("const", "outlier", "narrow"):
             shaped.append(([n], [max(1, n // 9)], 1 / 3, shape))
-    cases = [c + ("mixed",) for c in cases] + shaped
+    return [c + ("mixed",) for c in cases] + shaped
+
+
+def _select_keys(rng, shape, total):
+    if shape == "mixed":
+        # keys drawn from small value sets plant exact ties, and include -0.0/+0.0
+        ki = rng.choice(np.array([0.0, -0.0, 1.5, 2.25, -7.0, 3e-8, 1e30], np.float32), size=total)
+        ki = np.where(rng.random(total) < 0.5, ki, rng.standard_normal(total).astype(np.float32))
+        ks = rng.choice(np.array([-1.0, -0.0, 0.0, 0.5, 0.25, 1.0], np.float32), size=total)
+        ks = np.where(rng.random(total) < 0.5, ks, rng.uniform(-1, 1, total).astype(np.float32))
+    elif shape == "const":
+        ki = np.full(total, 0.75, np.float32)
+        ks = np.full(total, -0.125, np.float32)
+    elif shape == "outlier":
+        ki = (0.57 + 1e-4 * rng.standard_normal(total)).astype(np.float32)
+        ki[total // 2] = 4095.0
+        ks = (0.3 + 1e-3 * rng.standard_normal(total)).astype(np.float32)
+        ks[total // 3] = -1.0
+    else:
+        ki = (1.0 + 1e-6 * rng.integers(0, 40, total)).astype(np.float32)
+        ks = (0.5 + 1e-7 * rng.integers(0, 300, total)).astype(np.float32)
+    return ki, ks
+
+
+def _select_against_oracle(cases, rng, stride_real):
+    import paper_2607_13500_amd as tr
     for ci, (N, K, lam, shape) in enumerate(cases):
-        say("select keys case", ci, "B", len(N), "lam", lam, "shape", shape)
+        say("select keys case", ci, "B", len(N), "lam", lam, "shape", shape, "stride_real", stride_real)
         total = sum(N)
-        if shape == "mixed":
-            # keys drawn from small value sets plant exact ties, and include -0.0/+0.0
-            ki = rng.choice(np.array([0.0, -0.0, 1.5, 2.25, -7.0, 3e-8, 1e30], np.float32), size=total)
-            ki = np.where(rng.random(total) < 0.5, ki, rng.standard_normal(total).astype(np.float32))
-            ks = rng.choice(np.array([-1.0, -0.0, 0.0, 0.5, 0.25, 1.0], np.float32), size=total)
-            ks = np.where(rng.random(total) < 0.5, ks, rng.uniform(-1, 1, total).astype(np.float32))
-        elif shape == "const":
-            ki = np.full(total, 0.75, np.float32)
-            ks = np.full(total, -0.125, np.float32)
-        elif shape == "outlier":
-            ki = (0.57 + 1e-4 * rng.standard_normal(total)).astype(np.float32)
-            ki[total // 2] = 4095.0
-            ks = (0.3 + 1e-3 * rng.standard_normal(total)).astype(np.float32)
-            ks[total // 3] = -1.0
-        else:
-            ki = (1.0 + 1e-6 * rng.integers(0, 40, total)).astype(np.float32)
-            ks = (0.5 + 1e-7 * rng.integers(0, 300, total)).astype(np.float32)
+        ki, ks = _select_keys(rng, shape, total)
         r = tr.Reducer(8, 8, torch.bfloat16, lam=lam, max_images=len(N), max_tokens=total,
-                       max_N=max(N))
+                       max_N=max(N), stride_real=stride_real)
         idx, src = r.select(torch.from_numpy(ki).to(DEV), torch.from_numpy(ks).to(DEV), N, K)
         idx, src = idx.cpu().numpy(), src.cpu().numpy()
         r0 = o0 = 0
         for n, k in zip(N, K):
             # Stage I key: smaller is more important, so the oracle ranks -key.
             wi, ws = oracle.select(-ki[r0:r0 + n].astype(np.float64), ks[r0:r0 + n].astype(np.float64),
-                                   k, lam)
+                                   k, lam, stride_mode=1 if stride_real else 0)
             assert np.array_equal(idx[o0:o0 + k], wi), (ci, n, k, lam)
             assert np.array_equal(src[o0:o0 + k], ws), (ci, n, k, lam)
             r0 += n
             o0 += k
         r.close()
+
+
+def test_select_bit_exact_on_given_keys():
+    """Integer work: with the same fp32 keys, the GPU selection equals the oracle's exactly."""
+    rng = np.random.default_rng(11)
+    _select_against_oracle(_select_cases(rng), rng, stride_real=False)
+
+
+def test_select_bit_exact_stride_real():
+    """The real-interval stride variant, on every selection path, equals the oracle's."""
+    rng = np.random.default_rng(12)
+    _select_against_oracle(_select_cases(rng, trials=30), rng, stride_real=True)
 
 
 def test_score_then_select_equals_reduce():
@@ -264,6 +282,100 @@ def test_capacity_and_max_n():
     for lam in (0.0, 1.0):
         w.lam, w.K = lam, [cap // 5]
         run_and_check(w)
+
+
+# ------------------------------------------- lambda extremes and stride variant
+
+LAM_CASES = [
+    ("llava", dict(B=4, N=576, D=4096, K=64)),
+    ("llava_fp32", dict()),
+    ("qwen_ragged", dict(B=4, n_lo=256, n_hi=6000, D=3584)),
+]
+
+
+@pytest.mark.parametrize("lam", [0.0, 1.0])
+@pytest.mark.parametrize("name,kw", LAM_CASES, ids=[n for n, _ in LAM_CASES])
+def test_lambda_extremes_skip_unused_scores(name, kw, lam):
+    """lambda = 1 never reads X_pre/X_post (passed as NULL); lambda = 0 never
+    scores X.  The kept set equals both the oracle's and that of a call that
+    computes both scores."""
+    say("lambda fast path", name, kw, "lam", lam)
+    w = synth.make(name, device=DEV, **kw)
+    w.lam = lam
+    r = reducer_for(w)
+    full = r.reduce(w.X, w.Xpre, w.Xpost, w.N, w.K, want_scores=True)
+    states = (None, None) if lam == 1.0 else (w.Xpre, w.Xpost)
+    fast = r.reduce(w.X, *states, w.N, w.K)
+    torch.cuda.synchronize()
+    assert fast.h2 is None and fast.s is None
+    assert torch.equal(full.idx, fast.idx) and torch.equal(full.src, fast.src)
+    assert torch.equal(full.out, fast.out)
+    rep = parity.check(w, fast, parity.oracle_reference(w))
+    print("   ", w.name, "lam", lam, rep.summary(), flush=True)
+    assert rep.ok(), rep.failures[:5]
+    if lam == 1.0:
+        assert rep.picks == 0
+    r.close()
+
+
+@pytest.mark.parametrize("D,Dc,dtype", [(4096, 4096, torch.bfloat16), (37, 45, torch.float32),
+                                        (3584, 1024, torch.bfloat16)])
+def test_partial_scores_are_bit_identical(D, Dc, dtype):
+    import paper_2607_13500_amd as tr
+    from paper_2607_13500_amd import _lib
+    say("partial scores", D, Dc, dtype)
+    w = _edge_workload(D, Dc, dtype, EDGE_KINDS, 300)
+    r = reducer_for(w)
+    cv2, s, h2 = r.score(w.X, w.Xpre, w.Xpost, want_h2=True)
+    cv2a, sa, h2a = r.score(w.X, None, None, want_h2=True)
+    cv2b, sb, h2b = r.score(None, w.Xpre, w.Xpost, want_h2=True)
+    torch.cuda.synchronize()
+    assert sa is None and cv2b is None and h2b is None
+    assert torch.equal(cv2, cv2a) and torch.equal(h2, h2a) and torch.equal(s, sb)
+    # a group given in part is rejected before anything is enqueued
+    lib = _lib.load()
+    p = lambda t: None if t is None else t.data_ptr()
+    for args in ((w.X, None, w.Xpost, cv2, s), (w.X, w.Xpre, w.Xpost, None, s),
+                 (None, w.Xpre, w.Xpost, cv2, s), (None, None, None, None, None)):
+        st = lib.tr_score(r._ctx, *[p(a) for a in args[:3]], w.X.shape[0], p(args[3]), p(args[4]),
+                          None, None)
+        assert st == _lib.TR_EINVAL, args
+    # lambda = 1/3 needs the MLP states: NULL is an argument error
+    with pytest.raises(tr.TRError):
+        r.reduce(w.X, None, None, w.N, w.K)
+    # asking for s needs them too, whatever lambda is
+    r1 = tr.Reducer(D, Dc, dtype, lam=1.0, max_images=1, max_tokens=300, max_N=300)
+    with pytest.raises(tr.TRError):
+        r1.reduce(w.X, None, None, w.N, w.K, want_scores=True)
+    r1.close()
+    r.close()
+
+
+STRIDE_CASES = [
+    ("llava", dict(B=4, N=576, D=4096, K=64)),
+    ("llava_next", dict(B=2, D=4096, K=320)),
+    ("qwen_ragged", dict(B=4, n_lo=256, n_hi=9000, D=3584)),
+    ("video", dict(B=1, frames=8, positions=576, D=1024, K=288)),     # N = 4608: split selection
+]
+
+
+@pytest.mark.parametrize("name,kw", STRIDE_CASES, ids=[n for n, _ in STRIDE_CASES])
+def test_stride_real_variant_parity(name, kw):
+    say("stride real", name, kw)
+    w = synth.make(name, device=DEV, **kw)
+    r = reducer_for(w, stride_real=True)
+    res = r.reduce(w.X, w.Xpre, w.Xpost, w.N, w.K, want_scores=True)
+    cv2, _, _ = r.score(w.X, None, None)
+    ref = parity.oracle_reference(w, stride_mode=1)
+    rep = parity.check(w, res, ref, cv2_gpu=cv2, stride_mode=1)
+    print("   ", w.name, "stride real", rep.summary(), flush=True)
+    assert rep.ok(), rep.failures[:5]
+    assert rep.stage2_near <= max(4, rep.picks // 100)
+    # the variant differs from Algorithm 1 wherever R / K2 is not an integer
+    base = reducer_for(w).reduce(w.X, w.Xpre, w.Xpost, w.N, w.K)
+    torch.cuda.synchronize()
+    assert not torch.equal(base.idx, res.idx)
+    r.close()
 
 
 # ---------------------------------------------------------------- full sizes
