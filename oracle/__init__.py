@@ -48,9 +48,13 @@ def _load():
     global _lib
     if _lib is not None:
         return _lib
-    if not os.path.exists(_LIB):
+    # ALTR_ORACLE_LIB names another build of altr_oracle.c to load instead;
+    # the mutation test uses it to run the pins against deliberately broken
+    # copies of the oracle.
+    path = os.environ.get("ALTR_ORACLE_LIB") or _LIB
+    if path == _LIB and not os.path.exists(_LIB):
         build(force=True)
-    lib = ctypes.CDLL(_LIB)
+    lib = ctypes.CDLL(path)
     vp, i32, i64, dbl = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_double
     lib.altr_oracle_renyi2.argtypes = [vp, i32, i32]
     lib.altr_oracle_renyi2.restype = dbl
