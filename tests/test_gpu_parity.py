@@ -284,6 +284,46 @@ def test_capacity_and_max_n():
         run_and_check(w)
 
 
+# ------------------------------------------------------ stream ordering
+
+ORDER_CASES = [
+    ("llava", dict(B=64, N=576, D=4096, K=64)),
+    ("qwen_ragged", dict(B=9, n_lo=256, n_hi=9000, D=1024)),
+    ("video", dict(B=3, frames=8, positions=576, D=512, K=288)),       # split selection
+]
+
+
+@pytest.mark.parametrize("name,kw", ORDER_CASES, ids=[n for n, _ in ORDER_CASES])
+def test_reduce_is_ordered_on_the_callers_stream(name, kw):
+    """Work the caller enqueues on its stream right after tr_reduce, with no
+    host synchronisation, sees the finished outputs: on the null stream and on
+    a stream of the caller's own, for back-to-back calls, and equal to the run
+    with the per-stage timing events."""
+    say("stream order", name, kw)
+    w = synth.make(name, device=DEV, **kw)
+    say("   rows", sum(w.N), "images", w.B)
+    r = reducer_for(w)
+    r.timing(True)
+    ref_run = r.reduce(w.X, w.Xpre, w.Xpost, w.N, w.K, want_scores=True)
+    torch.cuda.synchronize()
+    r.timing_read()
+    r.timing(False)
+    for stream in (torch.cuda.current_stream(), torch.cuda.Stream()):
+        with torch.cuda.stream(stream):
+            copies = []
+            for _ in range(3):
+                res = r.reduce(w.X, w.Xpre, w.Xpost, w.N, w.K, want_scores=True)
+                copies.append([t.clone() for t in res])
+        torch.cuda.synchronize()
+        for c in copies:
+            for u, v in zip(ref_run, c):
+                assert torch.equal(u, v)
+    rep = parity.check(w, ref_run, parity.oracle_reference(w))
+    print("   ", w.name, rep.summary(), flush=True)
+    assert rep.ok(), rep.failures[:5]
+    r.close()
+
+
 # ------------------------------------------- lambda extremes and stride variant
 
 LAM_CASES = [
