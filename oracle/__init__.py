@@ -11,6 +11,8 @@ per definition):
 * Eq. (6): cosine between the pre- and post-MLP states of a token.
 * Algorithm 1 / Eq. (7): budget split, top-K1 by entropy, ascending sort of
   the remainder by the cosine, stride picks, union in ascending token index.
+* Variants: Shannon entropy of the same distribution as the Stage I score;
+  the real-valued stride interval of the method's prose.
 
 This module only marshals numpy arrays into that library and builds it with
 gcc when it is missing.  Parity pins: ``tests/test_oracle_pins.py``.
@@ -62,14 +64,16 @@ def _load():
     lib.altr_oracle_renyi2_cv.restype = dbl
     lib.altr_oracle_cosine.argtypes = [vp, vp, i32, i32]
     lib.altr_oracle_cosine.restype = dbl
-    lib.altr_oracle_scores.argtypes = [vp, vp, vp, i32, i64, i32, i32, vp, vp]
+    lib.altr_oracle_shannon.argtypes = [vp, i32, i32]
+    lib.altr_oracle_shannon.restype = dbl
+    lib.altr_oracle_scores.argtypes = [vp, vp, vp, i32, i64, i32, i32, i32, vp, vp]
     lib.altr_oracle_scores.restype = None
     lib.altr_oracle_budget.argtypes = [i32, i32, dbl, vp, vp, vp]
     lib.altr_oracle_budget.restype = i32
     lib.altr_oracle_select.argtypes = [i32, i32, dbl, vp, vp, vp, i32, vp, vp]
     lib.altr_oracle_select.restype = i32
     lib.altr_oracle_reduce.argtypes = [vp, vp, vp, i32, i32, vp, vp, i32, i32, dbl,
-                                       i32, vp, vp, vp, vp, vp, vp]
+                                       i32, i32, vp, vp, vp, vp, vp, vp]
     lib.altr_oracle_reduce.restype = i32
     _lib = lib
     return lib
@@ -118,6 +122,12 @@ def renyi2_cv(row) -> float:
     return _load().altr_oracle_renyi2_cv(_ptr(a), dt, a.size)
 
 
+def shannon(row) -> float:
+    """Shannon entropy -sum p log p of the Eq. (3) distribution (variant; all-zero row -> 0)."""
+    a, dt = as_raw(row)
+    return _load().altr_oracle_shannon(_ptr(a), dt, a.size)
+
+
 def cosine(a, b) -> float:
     """Eq. (6) for one token (zero norm -> 0)."""
     ra, dt = as_raw(a)
@@ -126,8 +136,12 @@ def cosine(a, b) -> float:
     return _load().altr_oracle_cosine(_ptr(ra), _ptr(rb), dt, ra.size)
 
 
-def scores(X, Xpre, Xpost):
-    """Per-row (H2, s) in float64 for packed [rows, D] / [rows, Dc] inputs."""
+def scores(X, Xpre, Xpost, entropy: int = 2):
+    """Per-row (H, s) in float64 for packed [rows, D] / [rows, Dc] inputs.
+
+    H is the Renyi-2 entropy (entropy=2, the method) or the Shannon entropy
+    (entropy=1, the variant).
+    """
     x, dt = as_raw(X)
     p, dt1 = as_raw(Xpre)
     q, dt2 = as_raw(Xpost)
@@ -137,7 +151,8 @@ def scores(X, Xpre, Xpost):
     assert p.shape == q.shape == (rows, Dc)
     h2 = np.empty(rows, np.float64)
     s = np.empty(rows, np.float64)
-    _load().altr_oracle_scores(_ptr(x), _ptr(p), _ptr(q), dt, rows, D, Dc, _ptr(h2), _ptr(s))
+    _load().altr_oracle_scores(_ptr(x), _ptr(p), _ptr(q), dt, rows, D, Dc, int(entropy),
+                               _ptr(h2), _ptr(s))
     return h2, s
 
 
@@ -173,12 +188,13 @@ def select(h2, s, K: int, lam: float, given_imp=None, stride_mode: int = 0):
 
 
 def reduce(X, Xpre, Xpost, N, K, lam: float, *, given_imp=None, stride_mode: int = 0,
-           want_out: bool = True, want_scores: bool = True):
+           entropy: int = 2, want_out: bool = True, want_scores: bool = True):
     """The whole module over a packed batch (Algorithm 1 per image).
 
     Returns a dict with ``idx`` (int32 [sum K], image-local), ``src``
     (uint8 [sum K]), ``out`` (kept rows of X, same raw dtype, or None),
-    ``h2`` / ``s`` (float64 [sum N], or None).
+    ``h2`` / ``s`` (float64 [sum N], or None; ``h2`` holds H1 when
+    ``entropy`` = 1, the Shannon variant).
     """
     x, dt = as_raw(X)
     p, _ = as_raw(Xpre)
@@ -196,7 +212,8 @@ def reduce(X, Xpre, Xpost, N, K, lam: float, *, given_imp=None, stride_mode: int
     s = np.empty(rows, np.float64) if want_scores else None
     gi = None if given_imp is None else np.ascontiguousarray(given_imp, dtype=np.uint8)
     rc = _load().altr_oracle_reduce(_ptr(x), _ptr(p), _ptr(q), dt, Na.size, _ptr(Na),
-                                    _ptr(Ka), D, Dc, float(lam), int(stride_mode), _ptr(gi),
+                                    _ptr(Ka), D, Dc, float(lam), int(stride_mode), int(entropy),
+                                    _ptr(gi),
                                     _ptr(idx), _ptr(src), _ptr(out), _ptr(h2), _ptr(s))
     if rc != 0:
         raise ValueError("oracle reduce failed on image %d" % (-rc - 1))

@@ -107,6 +107,28 @@ double altr_oracle_renyi2_cv(const void* row, int dtype, int D)
     return log((double)D) - log1p(v / (m * m));
 }
 
+/* ---- Variant: Shannon entropy of the same distribution ----------------- */
+
+/* H1(x) = -sum_j p_j log p_j with p_j = |x_j| / sum_k |x_k| (Eq. (3)) and
+ * 0 log 0 = 0; an all-zero row has H1 = 0, the same reading as for H2.  The
+ * paper names Shannon entropy only as the measure its Renyi score improves
+ * on (Sec. "Stage I"); it is a selectable variant of the Stage I score. */
+double altr_oracle_shannon(const void* row, int dtype, int D)
+{
+    double norm = 0.0;
+    for (int k = 0; k < D; ++k)
+        norm += fabs(elem(row, dtype, (size_t)k));
+    if (norm == 0.0)
+        return 0.0; /* reading: an all-zero row has H1 = 0 */
+    double h = 0.0;
+    for (int j = 0; j < D; ++j) {
+        double q = fabs(elem(row, dtype, (size_t)j)) / norm;
+        if (q > 0.0)
+            h -= q * log(q);
+    }
+    return h;
+}
+
 /* ---- Stage II: Eq. (6) ------------------------------------------------ */
 
 /* s = <a, b> / (||a||_2 ||b||_2); s = 0 when either norm is zero (reading).
@@ -128,15 +150,18 @@ double altr_oracle_cosine(const void* a, const void* b, int dtype, int Dc)
     return dot / sqrt(na * nb);
 }
 
-/* Per-token scores for a packed block of rows. */
+/* Per-token scores for a packed block of rows.  entropy selects the Stage I
+ * score: 2 = Renyi-2 (Eq. (4), the method), 1 = Shannon (the variant). */
 void altr_oracle_scores(const void* X, const void* Xpre, const void* Xpost,
-                        int dtype, int64_t rows, int D, int Dc,
+                        int dtype, int64_t rows, int D, int Dc, int entropy,
                         double* h2, double* s)
 {
     size_t eb = elem_bytes(dtype);
     for (int64_t i = 0; i < rows; ++i) {
+        const void* xr = (const char*)X + (size_t)i * D * eb;
         if (h2)
-            h2[i] = altr_oracle_renyi2((const char*)X + (size_t)i * D * eb, dtype, D);
+            h2[i] = entropy == 1 ? altr_oracle_shannon(xr, dtype, D)
+                                 : altr_oracle_renyi2(xr, dtype, D);
         if (s)
             s[i] = altr_oracle_cosine((const char*)Xpre + (size_t)i * Dc * eb,
                                       (const char*)Xpost + (size_t)i * Dc * eb,
@@ -284,11 +309,12 @@ int altr_oracle_select(int N, int K, double lambda, const double* h2,
  * image-local.  out (may be NULL) receives the kept rows of X byte for byte.
  * h2 and s (may be NULL) receive the per-token scores of all rows.
  * given_imp (may be NULL) is the packed per-token X^imp mask of the
- * conditional form.  Returns 0, or -(1 + b) for the first failing image. */
+ * conditional form.  entropy: 2 = Renyi-2 (the method), 1 = Shannon (h2 then
+ * receives H1).  Returns 0, or -(1 + b) for the first failing image. */
 int altr_oracle_reduce(const void* X, const void* Xpre, const void* Xpost,
                        int dtype, int B, const int32_t* N, const int32_t* K,
                        int D, int Dc, double lambda, int stride_mode,
-                       const uint8_t* given_imp, int32_t* out_idx,
+                       int entropy, const uint8_t* given_imp, int32_t* out_idx,
                        uint8_t* out_src, void* out, double* h2, double* s)
 {
     size_t eb = elem_bytes(dtype);
@@ -305,7 +331,7 @@ int altr_oracle_reduce(const void* X, const void* Xpre, const void* Xpost,
         altr_oracle_scores((const char*)X + (size_t)row0 * D * eb,
                            (const char*)Xpre + (size_t)row0 * Dc * eb,
                            (const char*)Xpost + (size_t)row0 * Dc * eb,
-                           dtype, n, D, Dc, hb, sb);
+                           dtype, n, D, Dc, entropy, hb, sb);
         if (h2) memcpy(h2 + row0, hb, sizeof(double) * (size_t)n);
         if (s) memcpy(s + row0, sb, sizeof(double) * (size_t)n);
         int rc = altr_oracle_select(n, K[b], lambda, hb, sb,

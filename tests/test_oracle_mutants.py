@@ -24,8 +24,12 @@ PINS = os.path.join(ROOT, "tests", "test_oracle_pins.py")
 MUTANTS = [
     # Eq. (3): the normaliser sums magnitudes
     ("normaliser_without_abs",
-     "        norm += fabs(elem(row, dtype, (size_t)k));",
-     "        norm += elem(row, dtype, (size_t)k);"),
+     "int D)\n{\n    double norm = 0.0;\n    for (int k = 0; k < D; ++k)\n"
+     "        norm += fabs(elem(row, dtype, (size_t)k));\n    if (norm == 0.0)\n"
+     "        return 0.0; /* reading: an all-zero row has H2 = 0 */",
+     "int D)\n{\n    double norm = 0.0;\n    for (int k = 0; k < D; ++k)\n"
+     "        norm += elem(row, dtype, (size_t)k);\n    if (norm == 0.0)\n"
+     "        return 0.0; /* reading: an all-zero row has H2 = 0 */"),
     # Eq. (4): the sum of squared probabilities
     ("probabilities_not_squared", "        sum_p2 += p * p;", "        sum_p2 += p;"),
     ("entropy_sign", "    return -log(sum_p2);", "    return log(sum_p2);"),
@@ -33,6 +37,18 @@ MUTANTS = [
     ("zero_row_reading",
      "        return 0.0; /* reading: an all-zero row has H2 = 0 */",
      "        return log((double)D);"),
+    # the Shannon variant
+    ("shannon_sign", "            h -= q * log(q);", "            h += q * log(q);"),
+    ("shannon_log_of_square", "            h -= q * log(q);", "            h -= q * log(q * q);"),
+    ("shannon_without_abs", "        double q = fabs(elem(row, dtype, (size_t)j)) / norm;",
+     "        double q = elem(row, dtype, (size_t)j) / norm;"),
+    ("shannon_normaliser_without_abs",
+     "        norm += fabs(elem(row, dtype, (size_t)k));\n    if (norm == 0.0)\n"
+     "        return 0.0; /* reading: an all-zero row has H1 = 0 */",
+     "        norm += elem(row, dtype, (size_t)k);\n    if (norm == 0.0)\n"
+     "        return 0.0; /* reading: an all-zero row has H1 = 0 */"),
+    ("entropy_variants_swapped", "            h2[i] = entropy == 1 ? altr_oracle_shannon(xr, dtype, D)",
+     "            h2[i] = entropy == 2 ? altr_oracle_shannon(xr, dtype, D)"),
     # bf16 widening
     ("bf16_shift", "        uint32_t w = ((uint32_t)h) << 16;", "        uint32_t w = ((uint32_t)h) << 15;"),
     # the variance form used as a self-check

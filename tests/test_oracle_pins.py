@@ -126,6 +126,71 @@ def test_h2_gaussian_row_statistics():
     assert 0.85 < h.std() / sd_pred < 1.15
 
 
+# ------------------------------------------- Shannon variant of the score
+
+@pytest.mark.parametrize("D", [1, 2, 7, 1024, 4096])
+def test_h1_closed_forms(D):
+    signs = RNG.choice([-1.0, 1.0], size=D)
+    for c in (1.0, 3.0, 1e-20):
+        for row in both_dtypes(c * signs):                     # uniform magnitude: log D
+            assert oracle.shannon(row) == pytest.approx(math.log(D), rel=1e-12, abs=1e-15)
+    row = np.zeros(D, np.float32)
+    row[D // 2] = -2.5
+    assert oracle.shannon(row) == 0.0                          # one-hot: 0
+    k = max(1, D // 3)
+    row = np.zeros(D, np.float32)
+    row[RNG.choice(D, size=k, replace=False)] = 0.75           # k equal non-zeros: log k
+    assert oracle.shannon(row) == pytest.approx(math.log(k), rel=1e-12, abs=1e-15)
+    assert oracle.shannon(np.zeros(D, np.float32)) == 0.0      # all-zero row: the H2 reading
+
+
+def test_h1_against_scipy_entropy():
+    import scipy.stats
+    for D in (2, 3, 64, 1000, 4096):
+        for kind in range(4):
+            if kind == 0:
+                x = RNG.standard_normal(D)
+            elif kind == 1:
+                x = 1.7 * (1 + 1e-3 * RNG.standard_normal(D))
+            elif kind == 2:
+                x = RNG.standard_t(3, D)
+            else:
+                x = np.where(RNG.random(D) < 0.05, 50.0, 0.0) * RNG.standard_normal(D)
+                x[0] = 1.0
+            for r in both_dtypes(x.astype(np.float32)):
+                a = np.abs(oracle.as_raw(r)[0].astype(np.float64)) if r.dtype == np.float32 \
+                    else np.abs(bf16_to_f32(r).astype(np.float64))
+                want = scipy.stats.entropy(a)               # normalises, natural log, 0 log 0 = 0
+                assert oracle.shannon(r) == pytest.approx(want, rel=1e-12, abs=1e-13)
+
+
+def test_h1_renyi_order_and_invariances():
+    # Renyi entropies do not increase with the order: H2 <= H1 <= log D, with
+    # equality only for a uniform magnitude distribution over the support.
+    for D in (5, 300, 4096):
+        x = (RNG.standard_normal(D) * RNG.lognormal(0, 1, D)).astype(np.float32)
+        h1, h2 = oracle.shannon(x), oracle.renyi2(x)
+        assert h2 < h1 < math.log(D)
+        assert oracle.shannon(np.float32(-4.0) * x) == pytest.approx(h1, rel=1e-12)
+        assert oracle.shannon(RNG.permutation(x)) == pytest.approx(h1, rel=1e-12)
+        assert oracle.shannon(x * RNG.choice([-1, 1], size=D).astype(np.float32)) == pytest.approx(h1, rel=1e-12)
+
+
+def test_h1_drives_stage1_in_the_variant():
+    # With entropy=1 the oracle's scores are H1 per row and lambda = 1 keeps
+    # the K highest-H1 tokens (numpy lexsort on (index, -H1)).
+    N, D, K = 300, 64, 40
+    X = (RNG.standard_normal((N, D)) * RNG.lognormal(0, 1, (N, 1))).astype(np.float32)
+    X[::7] = np.abs(X[::7]).mean()                            # planted exact ties (uniform rows)
+    P = RNG.standard_normal((N, D)).astype(np.float32)
+    h1, s = oracle.scores(X, P, P, entropy=1)
+    assert np.array_equal(h1, np.array([oracle.shannon(r) for r in X]))
+    ref = oracle.reduce(X, P, P, [N], [K], 1.0, entropy=1)
+    want = np.sort(np.lexsort((np.arange(N), -h1))[:K])
+    assert np.array_equal(ref["idx"], want)
+    assert np.array_equal(ref["h2"], h1)
+
+
 # ---------------------------------------------------------------- Eq. (6)
 
 def test_cosine_closed_forms():
