@@ -44,6 +44,8 @@ def parse():
                          "the score they do not use")
     ap.add_argument("--stride-real", action="store_true",
                     help="real-interval variant of the diversity stride")
+    ap.add_argument("--shannon", action="store_true",
+                    help="Shannon-entropy variant of the Stage I score")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="target wall time of the oracle sample")
@@ -86,7 +88,7 @@ def describe(w) -> str:
     return "%s, %d x %s tokens x %d %s -> %s kept" % (kind, w.B, ns, w.D, dt, ks)
 
 
-def cpu_baseline(w, seconds: float):
+def cpu_baseline(w, seconds: float, entropy: int = 2, stride_mode: int = 0):
     import oracle
     # a bounded sample: the first images up to ~40k tokens, repeated to ~`seconds`
     nb, rows = 0, 0
@@ -97,7 +99,8 @@ def cpu_baseline(w, seconds: float):
     runs = 0
     t0 = time.perf_counter()
     while True:
-        oracle.reduce(X, P, Q, w.N[:nb], w.K[:nb], w.lam, want_out=True, want_scores=False)
+        oracle.reduce(X, P, Q, w.N[:nb], w.K[:nb], w.lam, want_out=True, want_scores=False,
+                      entropy=entropy, stride_mode=stride_mode)
         runs += 1
         el = time.perf_counter() - t0
         if el >= seconds or runs >= 50:
@@ -128,10 +131,10 @@ def main():
     if args.lam is not None:
         w.lam = float(args.lam)
     headline = (args.workload == "llava" and args.images == 64 and args.K == 64
-                and w.lam == synth.LAMBDA and not args.stride_real)
+                and w.lam == synth.LAMBDA and not args.stride_real and not args.shannon)
     torch.cuda.synchronize()
     r = tr.Reducer(w.D, w.Dc, w.dtype, lam=w.lam, max_images=w.B, max_tokens=sum(w.N),
-                   max_N=max(w.N), stride_real=args.stride_real)
+                   max_N=max(w.N), stride_real=args.stride_real, shannon=args.shannon)
     # Which scores the plan needs (the library decides the same way): H2 unless
     # lambda = 0, s unless lambda = 1.  A score that is not needed is not read.
     plan = tr.plan(w.N, w.K, w.lam)
@@ -196,9 +199,10 @@ def main():
     traffic = measured_traffic() if headline else None
 
     line = {
-        "metric": METRIC if headline else "images/s (%s workload%s%s)" % (
+        "metric": METRIC if headline else "images/s (%s workload%s%s%s)" % (
             args.workload, "" if w.lam == synth.LAMBDA else ", lambda=%g" % w.lam,
-            ", real-interval stride" if args.stride_real else ""),
+            ", real-interval stride" if args.stride_real else "",
+            ", Shannon entropy" if args.shannon else ""),
         "value": round(images_s, 1),
         "unit": "images/s",
         "n_gpus": 1,
@@ -214,6 +218,7 @@ def main():
                    "images": w.B, "tokens": rows, "D": w.D, "Dc": w.Dc, "kept": sum(w.K),
                    "lambda": round(w.lam, 6),
                    "stride": "real-interval" if args.stride_real else "algorithm-1",
+                   "entropy": "shannon" if args.shannon else "renyi-2",
                    "scores": "+".join(n for n, f in (("H2", need_x), ("s", need_s)) if f)},
         "tokens_per_s": round(rows * args.steps / elapsed, 1),
         "path_hbm": {"algorithmic_bytes": path_bytes,
@@ -228,7 +233,8 @@ def main():
                      "traffic": traffic, "algorithmic_bytes_per_launch": score_bytes},
     }
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+        line["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds, 1 if args.shannon else 2,
+                                            1 if args.stride_real else 0)
     r.close()
     print(json.dumps(line), flush=True)
     if args.calib_copy_mib > 0:

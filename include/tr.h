@@ -76,7 +76,14 @@ typedef enum {
      * method's prose states (Sec. "Methodology", diversity stage) instead of
      * Algorithm 1's integer stride: X^div = sorted positions floor(j R / K2),
      * j = 0 .. K2-1, which spreads the picks over the whole of X^rem. */
-    TR_FLAG_STRIDE_REAL = 1
+    TR_FLAG_STRIDE_REAL = 1,
+    /* Stage I ranks by the Shannon entropy H1 = -sum_j p_j log p_j of the
+     * same distribution p (Eq. (3); 0 log 0 = 0, an all-zero row has H1 = 0)
+     * instead of Eq. (4)'s Renyi-2 entropy: the measure the paper names as
+     * the one its score improves on (Sec. "Stage I").  The Stage I key is
+     * then KL = log D - H1 (ascending = descending H1) and out_h2 receives
+     * H1.  Costs a logarithm per element of X. */
+    TR_FLAG_SHANNON = 2
 } tr_flag;
 
 /* Problem statement and capacities, fixed for the life of a context. */
@@ -112,7 +119,8 @@ tr_status tr_create(const tr_params* p, tr_ctx** out);
  *   out_idx device int32 [sum K] kept token indices, image-local, strictly
  *          ascending within an image
  *   out_src device uint8 [sum K] or NULL: 0 = kept by Stage I, 1 = Stage II
- *   out_h2 device float [sum N] or NULL: H2 of every token (nats)
+ *   out_h2 device float [sum N] or NULL: H2 of every token (nats; H1 with
+ *          TR_FLAG_SHANNON)
  *   out_s  device float [sum N] or NULL: s of every token
  *   stream hipStream_t or NULL
  * X, X_pre, X_post and out may have any alignment (16-byte aligned bases and
@@ -135,9 +143,11 @@ tr_status tr_reduce(tr_ctx* ctx, const void* X, const void* X_pre,
  * the same kernel and bit-identical results as inside tr_reduce.
  *   key_imp device float [rows]: the Stage I key CV^2 = Var|x| / mean|x|^2
  *           (population variance over the D channels), D - 1 for an all-zero
- *           row; ascending CV^2 is descending H2
+ *           row; ascending CV^2 is descending H2.  With TR_FLAG_SHANNON:
+ *           KL = log D - H1 (log D for an all-zero row)
  *   key_s   device float [rows]: s (Eq. 6)
- *   out_h2  device float [rows] or NULL: H2 = log D - log1p(CV^2)
+ *   out_h2  device float [rows] or NULL: H2 = log D - log1p(CV^2) (with
+ *           TR_FLAG_SHANNON: H1 = log D - KL)
  * Either score may be left out: X, key_imp (and out_h2) all NULL computes s
  * alone; X_pre, X_post and key_s all NULL computes the Stage I key alone.
  * A partly given group, or nothing to compute, is TR_EINVAL.

@@ -88,13 +88,15 @@ class Reducer:
     """A library context bound to one device, row widths, dtype and lambda.
 
     stride_real selects the real-interval variant of the diversity stride
-    (positions floor(j R / K2) of the sorted remainder instead of j t).
+    (positions floor(j R / K2) of the sorted remainder instead of j t);
+    shannon ranks Stage I by Shannon entropy instead of Renyi-2 (the key is
+    then log D - H1 and the returned h2 holds H1).
     """
 
     def __init__(self, D: int, Dc: Optional[int] = None, dtype: torch.dtype = torch.bfloat16,
                  lam: float = LAMBDA_PAPER, keep_ratio: Optional[float] = None,
                  max_images: int = 256, max_tokens: int = 1 << 20, max_N: Optional[int] = None,
-                 device=None, stride_real: bool = False):
+                 device=None, stride_real: bool = False, shannon: bool = False):
         if not torch.cuda.is_available():
             raise RuntimeError("paper_2607_13500_amd needs a ROCm GPU (gfx950)")
         self.device = torch.device("cuda", torch.cuda.current_device() if device is None
@@ -105,9 +107,9 @@ class Reducer:
         if max_N is None:
             max_N = min(capacity_N_on(self.device), int(max_tokens))
         self.max_images, self.max_tokens, self.max_N = int(max_images), int(max_tokens), int(max_N)
-        self.stride_real = bool(stride_real)
-        p = _params(D, Dc, dtype, lam, keep_ratio, max_images, max_tokens, max_N,
-                    _lib.TR_FLAG_STRIDE_REAL if stride_real else 0)
+        self.stride_real, self.shannon = bool(stride_real), bool(shannon)
+        flags = (_lib.TR_FLAG_STRIDE_REAL if stride_real else 0) | (_lib.TR_FLAG_SHANNON if shannon else 0)
+        p = _params(D, Dc, dtype, lam, keep_ratio, max_images, max_tokens, max_N, flags)
         ctx = ctypes.c_void_p()
         with torch.cuda.device(self.device):
             _check(self.lib.tr_create(ctypes.byref(p), ctypes.byref(ctx)), "tr_create")

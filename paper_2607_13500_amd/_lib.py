@@ -34,6 +34,7 @@ class Params(ctypes.Structure):
 TR_OK, TR_EINVAL, TR_ENOMEM, TR_EUNSUPPORTED, TR_EDEVICE = range(5)
 TR_FP32, TR_BF16 = 0, 1
 TR_FLAG_STRIDE_REAL = 1
+TR_FLAG_SHANNON = 2
 
 _lib = None
 

@@ -1,0 +1,45 @@
+"""Coefficients of the polynomial the scoring kernel uses for the Shannon term.
+
+phi(e) = g(1 + e) / e^2 with g(u) = u log u - u + 1, on |e| <= 1/4, as a
+degree-7 polynomial in e: the Chebyshev interpolant at 2000 Chebyshev nodes
+(fp64), converted to monomial coefficients.  Prints the coefficients and the
+maximum relative error of phi over the interval (fp64 evaluation, then fp32
+Horner with fused multiply-adds).  Only numpy is needed.
+"""
+import numpy as np
+from numpy.polynomial import chebyshev
+
+A = 0.25
+DEG = 7
+
+
+def phi(e):
+    e = np.asarray(e, np.float64)
+    out = np.empty_like(e)
+    small = np.abs(e) < 1e-3
+    k = np.arange(2, 40)
+    out[small] = ((-e[small][:, None]) ** (k - 2) / (k * (k - 1))).sum(1)
+    eb = e[~small]
+    out[~small] = ((1 + eb) * np.log1p(eb) - eb) / eb ** 2
+    return out
+
+
+def fit():
+    nodes = np.cos(np.pi * (np.arange(2000) + 0.5) / 2000) * A
+    cheb = chebyshev.chebfit(nodes / A, phi(nodes), DEG)
+    return chebyshev.cheb2poly(cheb) / A ** np.arange(DEG + 1)
+
+
+if __name__ == "__main__":
+    p = fit()
+    grid = np.linspace(-A, A, 200001)
+    ref = phi(grid)
+    err64 = np.max(np.abs(np.polyval(p[::-1], grid) - ref) / ref)
+    acc = np.full(grid.size, np.float32(p[-1]))
+    g32 = grid.astype(np.float32)
+    for c in p[-2::-1]:
+        acc = (acc.astype(np.float64) * g32 + np.float64(np.float32(c))).astype(np.float32)
+    err32 = np.max(np.abs(acc - ref) / ref)
+    for i, c in enumerate(p):
+        print("c%d = %.9e" % (i, c))
+    print("max relative error: fp64 %.2e, fp32 Horner %.2e" % (err64, err32))

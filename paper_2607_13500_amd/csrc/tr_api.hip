@@ -47,7 +47,8 @@ tr_status check_params(const tr_params* p, bool need_caps)
     if (p->Dc < 0) return fail(TR_EINVAL, "Dc must be >= 0 (got %d)", p->Dc);
     if (p->dtype != TR_FP32 && p->dtype != TR_BF16)
         return fail(TR_EINVAL, "dtype must be TR_FP32 or TR_BF16 (got %d)", p->dtype);
-    if (p->flags & ~(int32_t)TR_FLAG_STRIDE_REAL) return fail(TR_EINVAL, "unknown flags 0x%x", p->flags);
+    if (p->flags & ~(int32_t)(TR_FLAG_STRIDE_REAL | TR_FLAG_SHANNON))
+        return fail(TR_EINVAL, "unknown flags 0x%x", p->flags);
     if (!(p->lambda >= 0.0 && p->lambda <= 1.0))
         return fail(TR_EINVAL, "lambda must be in [0, 1] (got %g)", p->lambda);
     if (!(p->keep_ratio == 0.0 || (p->keep_ratio > 0.0 && p->keep_ratio <= 1.0)))
@@ -410,7 +411,8 @@ tr_status tr_reduce(tr_ctx* c, const void* X, const void* X_pre, const void* X_p
     // H2 is asked for, Stage II's likewise (lambda = 1 never needs s, lambda
     // = 0 never needs H2).  A score that is not needed is not computed and its
     // inputs are not read.
-    const int mode = (pl.keys_imp || out_h2 ? tr::kScoreImp : 0) | (pl.keys_s || out_s ? tr::kScoreSim : 0);
+    int mode = (pl.keys_imp || out_h2 ? tr::kScoreImp : 0) | (pl.keys_s || out_s ? tr::kScoreSim : 0);
+    if ((mode & tr::kScoreImp) && (c->p.flags & TR_FLAG_SHANNON)) mode |= tr::kScoreShannon;
     const bool need_c = (mode & tr::kScoreSim) != 0;
     if (need_c && (!X_pre || !X_post))
         return fail(TR_EINVAL, "X_pre and X_post must be non-NULL when Stage II ranks tokens or out_s is set");
@@ -502,7 +504,8 @@ tr_status tr_score(tr_ctx* c, const void* X, const void* X_pre, const void* X_po
     sa.out_h2 = out_h2;
     sa.out_s = nullptr;
     sa.logD = (float)log((double)c->p.D);
-    const int mode = (want_x ? tr::kScoreImp : 0) | (want_c ? tr::kScoreSim : 0);
+    int mode = (want_x ? tr::kScoreImp : 0) | (want_c ? tr::kScoreSim : 0);
+    if (want_x && (c->p.flags & TR_FLAG_SHANNON)) mode |= tr::kScoreShannon;
     hipError_t e = tr::launch_score(sa, c->p.dtype == TR_BF16, vec, mode, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "score kernel launch");
     return TR_OK;

@@ -18,9 +18,9 @@ struct ScoreArgs {
     int64_t rows;
     int32_t D;
     int32_t Dc;
-    float* key_imp;      // [rows] CV^2 of |x| (Stage I key, ascending), or nullptr
+    float* key_imp;      // [rows] CV^2 of |x| (Shannon: log D - H1) (Stage I key, ascending), or nullptr
     float* key_s;        // [rows] s (Stage II key, ascending), or nullptr
-    float* out_h2;       // [rows] or nullptr
+    float* out_h2;       // [rows] H2 (Shannon: H1), or nullptr
     float* out_s;        // [rows] or nullptr
     float logD;          // log(D) in fp32
 };
@@ -30,6 +30,7 @@ struct ScoreArgs {
 // optional output is not written.
 constexpr int kScoreImp = 1;   // Eq. (3)-(4) from X: key_imp, out_h2
 constexpr int kScoreSim = 2;   // Eq. (6) from X_pre, X_post: key_s, out_s
+constexpr int kScoreShannon = 4;   // with kScoreImp: Shannon variant (key KL = log D - H1, out H1)
 
 // bf16: true for bfloat16 rows, false for fp32.  vec: every row start is
 // 16-byte aligned (vector loads); otherwise element loads with the same

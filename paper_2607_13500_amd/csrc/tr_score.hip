@@ -26,6 +26,18 @@
 // Stage II's alone): the other tensor is then never read and its key is
 // written as 0.  The scores that are computed are bit-identical to those of a
 // launch that computes both, because each score's arithmetic is independent.
+//
+// Shannon variant of Stage I (H1 = -sum p log p of the same p): the key is
+// KL = log D - H1 >= 0 (ascending = descending H1), accumulated without
+// cancellation as a sum of non-negative terms.  With u = |x| / c for the same
+// row shift c and g(u) = u log u - u + 1 >= 0, and r = mean|x| / c,
+//   D KL = sum_j (|x_j|/m) log(|x_j|/m) = (sum_j g(u_j) - D g(r)) / r,
+// where the subtracted D g(r) is small because c lies close to the mean.
+// Every u is formed as 1 + e with e = (|x| - c) (1/c) + delta, delta =
+// c (1/c) - 1 taken exactly by a fused multiply-add, so all terms (and r)
+// refer to the same effective shift 1 / (1/c) and e keeps full relative
+// accuracy for near-uniform rows.  A row whose probe mean is 0 uses the plain
+// form H1 = log S - (sum |x| log |x|) / S instead.
 #include "tr_internal.h"
 #include "tr_wave.h"
 
@@ -104,7 +116,7 @@ __device__ __forceinline__ void load_partial(const char* row, int c, int m, floa
 
 struct XAcc {
     float sd;    // sum (|x| - c)
-    float sd2;   // sum (|x| - c)^2
+    float sd2;   // sum (|x| - c)^2; Shannon: sum g(|x| / c) (or sum |x| log |x| when c = 0)
 };
 
 struct CAcc {
@@ -117,6 +129,52 @@ __device__ __forceinline__ void x_chunk(XAcc& a, const float* v, int m, float c)
         const float d = fabsf(v[k]) - c;
         a.sd += d;
         a.sd2 = fmaf(d, d, a.sd2);
+    }
+}
+
+// g(1 + e) = (1 + e) log(1 + e) - e >= 0, given e (and u = 1 + e for the
+// direct form).  For |e| < 1/4 as e^2 phi(e), phi a degree-7 polynomial (the
+// Chebyshev interpolant of g(1 + e) / e^2 on [-1/4, 1/4], relative error
+// 3e-9; coefficients from gen_shannon_poly.py), which keeps full relative
+// accuracy where the direct form cancels; elsewhere u log u - e with the
+// hardware base-2 logarithm (argument clamped to 1e-30, a normal number, so
+// u = 0 gives 0 - e = 1).  Both forms are evaluated and one is selected: no
+// per-element divergence.
+__device__ __forceinline__ float g_shannon(float e, float u)
+{
+    float p = -1.525888537e-02f;
+    p = fmaf(p, e, 1.933413531e-02f);
+    p = fmaf(p, e, -2.374382957e-02f);
+    p = fmaf(p, e, 3.327445834e-02f);
+    p = fmaf(p, e, -5.000115357e-02f);
+    p = fmaf(p, e, 8.333407677e-02f);
+    p = fmaf(p, e, -1.666666612e-01f);
+    p = fmaf(p, e, 4.999999985e-01f);
+    const float series = (e * e) * p;
+    constexpr float kLn2 = 0.693147180559945309f;
+    const float direct = fmaf(u * kLn2, __builtin_amdgcn_logf(fmaxf(u, 1e-30f)), -e);
+    return fabsf(e) < 0.25f ? series : direct;
+}
+
+// Shannon partial sums over m elements for a row shift c > 0 (inv = 1/c,
+// delta = c inv - 1): sd as for CV^2, sd2 = sum g(|x| / c).
+__device__ __forceinline__ void x_chunk_shannon(XAcc& a, const float* v, int m, float c, float inv,
+                                                float delta)
+{
+    for (int k = 0; k < m; ++k) {
+        const float ax = fabsf(v[k]);
+        a.sd += ax - c;
+        a.sd2 += g_shannon(fmaf(ax - c, inv, delta), ax * inv);
+    }
+}
+
+// The same for a row whose probe mean is 0: sd = sum |x|, sd2 = sum |x| log |x|.
+__device__ __forceinline__ void x_chunk_shannon_plain(XAcc& a, const float* v, int m)
+{
+    for (int k = 0; k < m; ++k) {
+        const float ax = fabsf(v[k]);
+        a.sd += ax;
+        a.sd2 = fmaf(ax * 0.693147180559945309f, __builtin_amdgcn_logf(fmaxf(ax, 1e-30f)), a.sd2);
     }
 }
 
@@ -185,6 +243,7 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a)
     constexpr int V = L::kV;
     constexpr bool kX = (MODE & kScoreImp) != 0;    // Eq. (3)-(4) over X
     constexpr bool kC = (MODE & kScoreSim) != 0;    // Eq. (6) over X_pre, X_post
+    constexpr bool kH1 = kX && (MODE & kScoreShannon) != 0;   // Shannon variant of Stage I
     const int lane = threadIdx.x & (kWave - 1);
     const int64_t row = (int64_t)blockIdx.x * (blockDim.x / kWave) + (threadIdx.x / kWave);
     if (row >= a.rows) return;   // whole wavefront leaves together
@@ -207,8 +266,24 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a)
 
     XAcc xa{0.f, 0.f};
     CAcc ca{0.f, 0.f, 0.f};
-    float c = 0.f;
-    if (kX && nfx == 0) c = wave_sum(tail_x ? abs_sum<V>(tx, mx) : 0.f) / n_probe;
+    float c = 0.f, inv_c = 0.f, delta = 0.f;
+    // 1/c and its exact rounding offset for the Shannon terms.
+    auto set_shift = [&](float cc) {
+        c = cc;
+        if constexpr (kH1) {
+            inv_c = c > 0.f ? 1.f / c : 0.f;
+            delta = c > 0.f ? fmaf(c, inv_c, -1.f) : 0.f;
+        }
+    };
+    auto x_acc = [&](const float* v, int m) {
+        if constexpr (kH1) {
+            if (c > 0.f) x_chunk_shannon(xa, v, m, c, inv_c, delta);   // c is wave-uniform
+            else x_chunk_shannon_plain(xa, v, m);
+        } else {
+            x_chunk(xa, v, m, c);
+        }
+    };
+    if (kX && nfx == 0) set_shift(wave_sum(tail_x ? abs_sum<V>(tx, mx) : 0.f) / n_probe);
 
     for (int j0 = 0; j0 < nf; j0 += kWave * UNR) {   // same trip count for every lane
         Raw rx[UNR], rp[UNR], rq[UNR];
@@ -230,7 +305,7 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a)
             } else if (tail_x) {
                 first = abs_sum<V>(tx, mx);
             }
-            c = wave_sum(first) / n_probe;
+            set_shift(wave_sum(first) / n_probe);
         }
 #pragma unroll
         for (int u = 0; u < UNR; ++u) {
@@ -238,12 +313,12 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a)
             if (ci < nfx) {
                 float v[V];
                 unpack<BF16>(rx[u], v);
-                x_chunk(xa, v, V, c);
+                x_acc(v, V);
             }
             if (ci < nfc) c_chunk<BF16>(ca, rp[u], rq[u]);
         }
     }
-    if (tail_x) x_chunk(xa, tx, mx, c);
+    if (tail_x) x_acc(tx, mx);
     if (kC && a.Dc % V && (nfc & (kWave - 1)) == lane) {
         const int m = a.Dc - nfc * V;
         c_chunk<BF16>(ca, load_partial_raw<BF16>(pr, nfc, m), load_partial_raw<BF16>(qr, nfc, m));
@@ -262,7 +337,24 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a)
 
     if (lane == 0) {
         float cv2 = 0.f, h2 = 0.f;
-        if constexpr (kX) {
+        if constexpr (kH1) {
+            // cv2 holds the key KL = log D - H1, h2 holds H1.
+            const float Df = (float)a.D;
+            const float mean = c + sd / Df;
+            if (!(mean > 0.f)) {   // all-zero row: H1 = 0
+                cv2 = a.logD;
+                h2 = 0.f;
+            } else if (c > 0.f) {
+                const float rm1 = fmaf(sd / Df, inv_c, delta);   // r - 1
+                const float r = 1.f + rm1;
+                const float dkl = (sd2 - Df * g_shannon(rm1, r)) / r;
+                cv2 = fmaxf(0.f, dkl / Df);
+                h2 = a.logD - cv2;
+            } else {   // probe mean 0: sd = sum |x|, sd2 = sum |x| log |x|
+                h2 = fmaxf(0.f, __logf(sd) - sd2 / sd);
+                cv2 = fmaxf(0.f, a.logD - h2);
+            }
+        } else if constexpr (kX) {
             const float Df = (float)a.D;
             const float mean = c + sd / Df;
             const float m2 = fmaxf(0.f, fmaf(-sd, sd / Df, sd2));
@@ -295,17 +387,23 @@ hipError_t launch_t(const ScoreArgs& a, hipStream_t s)
     constexpr int kRowsPerBlock = kThreads / kWave;
     const int64_t blocks = (a.rows + kRowsPerBlock - 1) / kRowsPerBlock;
     if (blocks <= 0) return hipSuccess;
-    hipLaunchKernelGGL((score_kernel<BF16, VEC, 4, MODE>), dim3((unsigned)blocks), dim3(kThreads), 0, s, a);
+    // The Shannon terms need more registers per element: half the loads in
+    // flight keeps 8 wavefronts per SIMD without spilling.
+    constexpr int kUnroll = (MODE & kScoreShannon) ? 2 : 4;
+    hipLaunchKernelGGL((score_kernel<BF16, VEC, kUnroll, MODE>), dim3((unsigned)blocks), dim3(kThreads), 0, s, a);
     return hipGetLastError();
 }
 
 template <bool BF16, bool VEC>
 hipError_t launch_m(const ScoreArgs& a, int mode, hipStream_t s)
 {
+    constexpr int I = kScoreImp, S = kScoreSim, H = kScoreShannon;
     switch (mode) {
-    case kScoreImp: return launch_t<BF16, VEC, kScoreImp>(a, s);
-    case kScoreSim: return launch_t<BF16, VEC, kScoreSim>(a, s);
-    default: return launch_t<BF16, VEC, kScoreImp | kScoreSim>(a, s);
+    case I: return launch_t<BF16, VEC, I>(a, s);
+    case S: return launch_t<BF16, VEC, S>(a, s);
+    case I | S: return launch_t<BF16, VEC, I | S>(a, s);
+    case I | H: return launch_t<BF16, VEC, I | H>(a, s);
+    default: return launch_t<BF16, VEC, I | S | H>(a, s);
     }
 }
 
@@ -313,7 +411,9 @@ hipError_t launch_m(const ScoreArgs& a, int mode, hipStream_t s)
 
 hipError_t launch_score(const ScoreArgs& a, bool bf16, bool vec, int mode, hipStream_t s)
 {
-    if (mode != kScoreImp && mode != kScoreSim && mode != (kScoreImp | kScoreSim)) return hipErrorInvalidValue;
+    const int base = mode & ~kScoreShannon;
+    if (base != kScoreImp && base != kScoreSim && base != (kScoreImp | kScoreSim)) return hipErrorInvalidValue;
+    if ((mode & kScoreShannon) && !(mode & kScoreImp)) mode &= ~kScoreShannon;
     if (bf16) return vec ? launch_m<true, true>(a, mode, s) : launch_m<true, false>(a, mode, s);
     return vec ? launch_m<false, true>(a, mode, s) : launch_m<false, false>(a, mode, s);
 }

@@ -7,7 +7,9 @@ score gap is inside the window an fp32 score error of TOL can cross:
 
 * P1  scores: |CV^2_gpu - CV^2| <= TOL CV^2 (+1e-12), |H2_gpu - H2| <=
       TOL max(1, |H2|), |s_gpu - s| <= TOL max(1, |s|).  CV^2 = expm1(log D - H2)
-      is the quantity the GPU ranks Stage I by (same order as H2).
+      is the quantity the GPU ranks Stage I by (same order as H2).  Shannon
+      variant: the key is KL = log D - H1 (+1e-11, the oracle's own rounding
+      of a near-zero KL) and H1 takes H2's place.
 * P2  Stage I: the GPU's X^imp may differ from the oracle's only in tokens whose
       oracle CV^2 lies within 2 TOL of the boundary value (the K1-th smallest);
       each such token is a counted near-tie swap, anything else fails.
@@ -59,10 +61,11 @@ class Report:
                    self.raw_mismatch, len(self.failures)))
 
 
-def oracle_reference(w, want_out=False, stride_mode=0):
+def oracle_reference(w, want_out=False, stride_mode=0, entropy=2):
     """Run the oracle on CPU copies of a workload (the same bytes the GPU sees)."""
     return oracle.reduce(w.X.cpu(), w.Xpre.cpu(), w.Xpost.cpu(), w.N, w.K, w.lam,
-                         want_out=want_out, want_scores=True, stride_mode=stride_mode)
+                         want_out=want_out, want_scores=True, stride_mode=stride_mode,
+                         entropy=entropy)
 
 
 def stride_positions(R: int, K2: int, t: int, stride_mode: int = 0) -> np.ndarray:
@@ -75,7 +78,21 @@ def cv2_from_h2(h2: np.ndarray, D: int) -> np.ndarray:
     return np.expm1(math.log(D) - h2)
 
 
-def check(w, res, ref, cv2_gpu=None, tol: float = TOL, stride_mode: int = 0) -> Report:
+def stage1_key(h: np.ndarray, D: int, entropy: int = 2) -> np.ndarray:
+    """The GPU's ascending Stage I key from the oracle's entropy: CV^2 =
+    expm1(log D - H2) (Renyi-2), or KL = log D - H1 (Shannon variant)."""
+    if entropy == 2:
+        return cv2_from_h2(h, D)
+    return np.maximum(0.0, math.log(D) - h)
+
+
+# Absolute floor of the Stage I key comparison: the oracle's own rounding of
+# log D - H (fp64, sums over D terms) for keys near 0.
+KEY_FLOOR = {2: 1e-12, 1: 1e-11}
+
+
+def check(w, res, ref, cv2_gpu=None, tol: float = TOL, stride_mode: int = 0,
+          entropy: int = 2) -> Report:
     """Apply P1-P5 to a GPU ReduceResult against an oracle run.
 
     res.h2 / res.s may be None (a run that did not return scores); P1 then
@@ -84,7 +101,8 @@ def check(w, res, ref, cv2_gpu=None, tol: float = TOL, stride_mode: int = 0) -> 
     rep = Report()
     D = w.D
     h2o, so = ref["h2"], ref["s"]
-    cv2o = cv2_from_h2(h2o, D)
+    cv2o = stage1_key(h2o, D, entropy)
+    floor = KEY_FLOOR[entropy]
     rep.tokens = h2o.size
     sg = None
     if res.h2 is not None:
@@ -106,7 +124,7 @@ def check(w, res, ref, cv2_gpu=None, tol: float = TOL, stride_mode: int = 0) -> 
         dc = np.abs(cg - cv2o)
         rel = dc / np.maximum(cv2o, 1e-300)
         rep.max_rel_cv2 = float(np.where(cv2o > 0, rel, 0).max(initial=0))
-        bad = np.nonzero(dc > tol * cv2o + 1e-12)[0]
+        bad = np.nonzero(dc > tol * cv2o + floor)[0]
         if bad.size:
             rep.failures.append("P1 CV^2 outside tolerance at rows %s" % bad[:8].tolist())
 
@@ -143,7 +161,7 @@ def check(w, res, ref, cv2_gpu=None, tol: float = TOL, stride_mode: int = 0) -> 
         if K1 > 0:
             order = np.lexsort((np.arange(n), c))
             theta = c[order[K1 - 1]]
-            win = 2 * tol * theta + 2e-12
+            win = 2 * tol * theta + 2 * floor
             if K1 < n and abs(c[order[K1]] - theta) <= win:
                 rep.stage1_windows += 1
             diff = np.setxor1d(imp_g, imp_o)

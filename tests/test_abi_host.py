@@ -138,7 +138,7 @@ def test_create_rejects_bad_params_before_touching_a_device():
     good = dict(D=64, Dc=0, dtype=1, max_images=4, max_tokens=1024, max_N=512, flags=0,
                 lam=1 / 3, keep_ratio=0.0)
     bad = [dict(D=0), dict(Dc=-1), dict(dtype=7), dict(max_images=0), dict(max_tokens=0),
-           dict(max_tokens=1 << 31), dict(max_N=0), dict(flags=2), dict(flags=-1), dict(lam=2.0),
+           dict(max_tokens=1 << 31), dict(max_N=0), dict(flags=4), dict(flags=-1), dict(lam=2.0),
            dict(keep_ratio=-0.5)]
     for b in bad:
         p = _lib.Params(**{**good, **b})

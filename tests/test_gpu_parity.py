@@ -391,6 +391,53 @@ def test_partial_scores_are_bit_identical(D, Dc, dtype):
     r.close()
 
 
+SHANNON_CASES = [
+    ("llava_fp32", dict()),                                            # 10 % near-constant rows
+    ("llava", dict(B=6, N=576, D=4096)),
+    ("llava", dict(B=3, N=577, D=520, K=100)),
+    ("qwen_ragged", dict(B=4, n_lo=256, n_hi=5000, D=3584)),
+    ("video", dict(B=1, frames=8, positions=576, D=1024, K=288)),
+]
+
+
+@pytest.mark.parametrize("name,kw", SHANNON_CASES, ids=[f"{n}-{i}" for i, (n, _) in enumerate(SHANNON_CASES)])
+def test_shannon_variant_parity(name, kw):
+    say("shannon", name, kw)
+    w = synth.make(name, device=DEV, **kw)
+    r = reducer_for(w, shannon=True)
+    res = r.reduce(w.X, w.Xpre, w.Xpost, w.N, w.K, want_scores=True)
+    key, s2, h1 = r.score(w.X, w.Xpre, w.Xpost, want_h2=True)
+    key_only, _, h1_only = r.score(w.X, None, None, want_h2=True)
+    torch.cuda.synchronize()
+    assert torch.equal(h1, res.h2) and torch.equal(s2, res.s)
+    assert torch.equal(key, key_only) and torch.equal(h1, h1_only)
+    rep = parity.check(w, res, parity.oracle_reference(w, entropy=1), cv2_gpu=key, entropy=1)
+    print("   ", w.name, "shannon", rep.summary(), flush=True)
+    assert rep.ok(), rep.failures[:5]
+    assert rep.stage1_swaps <= max(1, rep.images // 10)
+    r.close()
+
+
+@pytest.mark.parametrize("D,Dc,dtype", [(4096, 4096, torch.bfloat16), (1024, 1024, torch.float32),
+                                        (37, 45, torch.bfloat16), (5, 3, torch.float32),
+                                        (1, 1, torch.bfloat16)])
+def test_shannon_degenerate_rows(D, Dc, dtype):
+    say("shannon degenerate rows", D, Dc, dtype)
+    w = _edge_workload(D, Dc, dtype, EDGE_KINDS, 150)
+    r = reducer_for(w, shannon=True)
+    res = r.reduce(w.X, w.Xpre, w.Xpost, w.N, w.K, want_scores=True)
+    key, _, _ = r.score(w.X, None, None)
+    rep = parity.check(w, res, parity.oracle_reference(w, entropy=1), cv2_gpu=key, entropy=1)
+    print("   ", "edge shannon", rep.summary(), flush=True)
+    assert rep.ok(), rep.failures[:5]
+    h1 = res.h2.cpu().numpy()
+    if D > 1:
+        assert h1[0] == 0.0 and h1[8] == 0.0                       # all-zero rows
+        assert abs(h1[1]) < 1e-5                                    # one-hot (log D - KL in fp32)
+        assert abs(h1[2] - math.log(D)) < 1e-5 * math.log(D)        # uniform magnitude
+    r.close()
+
+
 STRIDE_CASES = [
     ("llava", dict(B=4, N=576, D=4096, K=64)),
     ("llava_next", dict(B=2, D=4096, K=320)),
@@ -430,6 +477,8 @@ FULL = [
     ("video", dict(), False),
 ]
 
+FULL_SHANNON = [("llava", dict(K=64), False), ("qwen_ragged", dict(), True)]
+
 
 @pytest.mark.parametrize("name,kw,ratio", FULL, ids=[f"{n}-{kw.get('K', '')}" for n, kw, _ in FULL])
 def test_reduce_parity_full(name, kw, ratio):
@@ -440,3 +489,17 @@ def test_reduce_parity_full(name, kw, ratio):
     # near-tie excusals must stay rare
     assert rep.stage1_swaps <= max(2, rep.images // 10)
     assert rep.stage2_near <= max(4, rep.picks // 100)
+
+
+@pytest.mark.parametrize("name,kw,ratio", FULL_SHANNON, ids=[n for n, _, _ in FULL_SHANNON])
+def test_shannon_parity_full(name, kw, ratio):
+    say("full shannon", name, kw)
+    w = synth.make(name, device=DEV, **kw)
+    r = reducer_for(w, shannon=True)
+    res = r.reduce(w.X, w.Xpre, w.Xpost, w.N, None if ratio else w.K, want_scores=True)
+    key, _, _ = r.score(w.X, None, None)
+    rep = parity.check(w, res, parity.oracle_reference(w, entropy=1), cv2_gpu=key, entropy=1)
+    print("   ", w.name, "shannon", rep.summary(), flush=True)
+    assert rep.ok(), rep.failures[:5]
+    assert rep.stage1_swaps <= max(2, rep.images // 10)
+    r.close()
