@@ -46,6 +46,14 @@ def parse():
                     help="real-interval variant of the diversity stride")
     ap.add_argument("--shannon", action="store_true",
                     help="Shannon-entropy variant of the Stage I score")
+    ap.add_argument("--mlp-fused", action="store_true",
+                    help="the step before the path: X_post from the encoder MLP's second layer "
+                         "(Dc = 1024, hidden 4096) with Eq. 6 fused into its epilogue, then the "
+                         "module on the given key; timed against the library GEMM + tr_reduce")
+    ap.add_argument("--project", type=int, default=0, metavar="NOUT",
+                    help="the step after the path: project the kept tokens by a [NOUT, D] weight "
+                         "inside the module (gather fused into the GEMM); timed against "
+                         "tr_reduce + the library GEMM")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="target wall time of the oracle sample")
@@ -110,6 +118,124 @@ def cpu_baseline(w, seconds: float, entropy: int = 2, stride_mode: int = 0):
                       % (runs, nb, w.B, rows, el)}
 
 
+def time_steps(torch, f, steps, warmup):
+    for _ in range(warmup):
+        f()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        f()
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) / steps
+
+
+def time_events(torch, f, steps, stream):
+    for _ in range(3):
+        f()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for _ in range(steps):
+        f()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    return ev0.elapsed_time(ev1) / steps * 1e-3
+
+
+def bench_fused(args, torch, synth, tr, dev):
+    """The two fusions around the path, each against its unfused form."""
+    w = synth.llava(device=dev, B=args.images, N=576, D=4096, K=args.K)
+    rows = sum(w.N)
+    g = torch.Generator(device=dev).manual_seed(7)
+    stream = torch.cuda.current_stream(dev)
+    line = {"n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "higher_is_better": True,
+            "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic"}
+    if args.mlp_fused:
+        Dc, Hd = 1024, 4096
+        Xpre = torch.randn(rows, Dc, device=dev, generator=g).to(torch.bfloat16)
+        H = torch.relu(torch.randn(rows, Hd, device=dev, generator=g) + 0.3).to(torch.bfloat16)
+        W2 = (torch.randn(Dc, Hd, device=dev, generator=g) / Hd ** 0.5).to(torch.bfloat16)
+        r = tr.Reducer(w.D, Dc, w.dtype, lam=w.lam, max_images=w.B, max_tokens=rows, max_N=576)
+        Xpost = torch.empty(rows, Dc, dtype=torch.bfloat16, device=dev)
+        sk = sum(w.K)
+        out = torch.empty(sk, w.D, dtype=w.dtype, device=dev)
+        idx = torch.empty(sk, dtype=torch.int32, device=dev)
+        src = torch.empty(sk, dtype=torch.uint8, device=dev)
+
+        def fused():
+            _, s = r.mlp_out_cos(H, W2, Xpre, out=Xpost)
+            r.reduce_given_s(w.X, s, w.N, w.K, out=out, out_idx=idx, out_src=src)
+
+        def unfused():
+            torch.matmul(H, W2.t(), out=Xpost)
+            r.reduce(w.X, Xpre, Xpost, w.N, w.K, out=out, out_idx=idx, out_src=src)
+
+        t_f = time_steps(torch, fused, args.steps, args.warmup)
+        t_u = time_steps(torch, unfused, args.steps, args.warmup)
+        t_gemm = time_events(torch, lambda: r.mlp_out_cos(H, W2, Xpre, out=Xpost), args.steps, stream)
+        t_lib = time_events(torch, lambda: torch.matmul(H, W2.t(), out=Xpost), args.steps, stream)
+        flops = 2.0 * rows * Dc * Hd
+        line.update({
+            "metric": "images/s: encoder MLP second layer with Eq. 6 fused + the module "
+                      "(64 x 576 tokens, Dc 1024, hidden 4096, X 4096 bf16 -> 64 kept)",
+            "value": round(w.B / t_f, 1), "unit": "images/s", "ms_per_step": round(t_f * 1e3, 5),
+            "config": {"workload": "llava-1.5 tokens with their CLIP-L last-MLP states, 64 x 576, "
+                                   "Dc 1024, hidden 4096, D 4096 bf16 -> 64 kept",
+                       "images": w.B, "tokens": rows, "D": w.D, "Dc": Dc, "hidden": Hd},
+            "unfused": {"ms_per_step": round(t_u * 1e3, 5), "value": round(w.B / t_u, 1),
+                        "what": "library GEMM (torch.matmul) + tr_reduce reading X_pre and X_post"},
+            "roofline": {"kernel": "gemm_kernel<cos epilogue> + cos_finish", "bound": "mfma",
+                         "achieved": round(flops / t_gemm / 1e12, 1), "avg_launch_ms": round(t_gemm * 1e3, 5),
+                         "peak": 2500.0, "unit": "TFLOP/s", "frac": round(flops / t_gemm / 1e12 / 2500.0, 4),
+                         "traffic": None, "algorithmic_flops_per_launch": flops,
+                         "library_gemm_ms": round(t_lib * 1e3, 5),
+                         "library_gemm_tflops": round(flops / t_lib / 1e12, 1)},
+        })
+        r.close()
+    else:
+        nout = args.project
+        r = tr.Reducer(w.D, w.Dc, w.dtype, lam=w.lam, max_images=w.B, max_tokens=rows, max_N=576)
+        W = (torch.randn(nout, w.D, device=dev, generator=g) / w.D ** 0.5).to(torch.bfloat16)
+        sk = sum(w.K)
+        out = torch.empty(sk, w.D, dtype=w.dtype, device=dev)
+        proj = torch.empty(sk, nout, dtype=torch.bfloat16, device=dev)
+        idx = torch.empty(sk, dtype=torch.int32, device=dev)
+        src = torch.empty(sk, dtype=torch.uint8, device=dev)
+
+        def fused():
+            r.reduce_project(w.X, w.Xpre, w.Xpost, w.N, w.K, W, out=proj, out_idx=idx, out_src=src)
+
+        def unfused():
+            r.reduce(w.X, w.Xpre, w.Xpost, w.N, w.K, out=out, out_idx=idx, out_src=src)
+            torch.matmul(out, W.t(), out=proj)
+
+        t_f = time_steps(torch, fused, args.steps, args.warmup)
+        t_u = time_steps(torch, unfused, args.steps, args.warmup)
+        r.reduce(w.X, w.Xpre, w.Xpost, w.N, w.K, out=out, out_idx=idx, out_src=src)
+        torch.cuda.synchronize()
+        t_gemm = time_events(torch, lambda: r.gemm(out, W, out=proj), args.steps, stream)
+        t_lib = time_events(torch, lambda: torch.matmul(out, W.t(), out=proj), args.steps, stream)
+        flops = 2.0 * sk * nout * w.D
+        line.update({
+            "metric": "images/s: the module with the projection of the kept tokens fused into its "
+                      "gather (64 x 576 x 4096 bf16 -> 64 kept, projected to %d)" % nout,
+            "value": round(w.B / t_f, 1), "unit": "images/s", "ms_per_step": round(t_f * 1e3, 5),
+            "config": {"workload": "llava-1.5 visual tokens, 64 x 576 x 4096 bf16 -> 64 kept -> "
+                                   "projected to %d" % nout,
+                       "images": w.B, "tokens": rows, "D": w.D, "kept": sk, "Nout": nout},
+            "unfused": {"ms_per_step": round(t_u * 1e3, 5), "value": round(w.B / t_u, 1),
+                        "what": "tr_reduce (gathered copy) + library GEMM (torch.matmul)"},
+            "roofline": {"kernel": "gemm_kernel<row gather>", "bound": "mfma",
+                         "achieved": round(flops / t_gemm / 1e12, 1), "avg_launch_ms": round(t_gemm * 1e3, 5),
+                         "peak": 2500.0, "unit": "TFLOP/s", "frac": round(flops / t_gemm / 1e12 / 2500.0, 4),
+                         "traffic": None, "algorithmic_flops_per_launch": flops,
+                         "library_gemm_ms": round(t_lib * 1e3, 5),
+                         "library_gemm_tflops": round(flops / t_lib / 1e12, 1)},
+        })
+        r.close()
+    print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -124,6 +250,9 @@ def main():
 
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
+    if args.mlp_fused or args.project:
+        bench_fused(args, torch, synth, tr, dev)
+        return
     if args.workload == "llava":
         w = synth.llava(device=dev, B=args.images, N=576, D=4096, K=args.K)
     else:

@@ -168,6 +168,60 @@ tr_status tr_select(tr_ctx* ctx, const float* key_imp, const float* key_s,
                     int32_t B, const int32_t* N, const int32_t* K,
                     int32_t* out_idx, uint8_t* out_src, void* stream);
 
+/* ---- The steps around the path, fused with it (bf16 contexts only) ------
+ *
+ * Matrix-core GEMM C[M, N] = A[M, K] . B[N, K]^T in bf16 with fp32
+ * accumulation and bf16 output (round to nearest even), the building block
+ * of the two entry points below.
+ *   A      device bf16, row m of the product is A + r * lda with r = m, or
+ *          r = a_rows[m] when a_rows (device int32 [M]) is given; rows
+ *          outside [0, a_row_count) read as zeros (memory-safe)
+ *   B      device bf16 [N, K] (row stride ldb), e.g. a Linear layer's weight
+ *   C      device bf16 [M, N] (row stride ldc)
+ * N must be a multiple of 128 and K of 64 (else TR_EUNSUPPORTED); A and B
+ * bases and row strides must be 16-byte aligned (else TR_EINVAL). */
+tr_status tr_gemm_bf16(tr_ctx* ctx, const void* A, int64_t lda,
+                       const int32_t* a_rows, int64_t a_row_count,
+                       const void* B, int64_t ldb, void* C, int64_t ldc,
+                       int32_t M, int32_t N, int32_t K, void* stream);
+
+/* The encoder MLP's second layer with Eq. (6) fused into its epilogue (Sec.
+ * "Stage II": x' and x'' are the input and output of the last MLP, Eq. 5):
+ *   X_post[M, Dc] = Hact[M, Hd] . W2[Dc, Hd]^T   (bf16 out, as tr_gemm_bf16)
+ *   key_s[M]      = cos(X_pre[m], X_post[m]) from the fp32 accumulators
+ * so the Stage II key is ready without another pass over X_pre or X_post.
+ *   Hact   device bf16 [M, Hd] hidden activations sigma(W1 x'), row stride ldh
+ *   W2     device bf16 [Dc, Hd], row stride ldw
+ *   X_pre  device bf16 [M, Dc] (x'), X_post device bf16 [M, Dc] (written)
+ *   key_s  device float [M] (written; zero norm -> 0)
+ * Dc is the context's; it must be a multiple of 128, Hd of 64; M <=
+ * max_tokens (the per-tile partial sums live in the context's scratch). */
+tr_status tr_mlp_out_cos(tr_ctx* ctx, const void* Hact, int64_t ldh,
+                         const void* W2, int64_t ldw, const void* X_pre,
+                         void* X_post, int32_t M, int32_t Hd, float* key_s,
+                         void* stream);
+
+/* tr_reduce with the Stage II key supplied (e.g. by tr_mlp_out_cos): X is
+ * scored for Stage I only, key_s (device float [sum N]) orders Stage II.
+ * Other arguments as tr_reduce. */
+tr_status tr_reduce_given_s(tr_ctx* ctx, const void* X, const float* key_s,
+                            int32_t B, const int32_t* N, const int32_t* K,
+                            void* out, int32_t* out_idx, uint8_t* out_src,
+                            float* out_h2, void* stream);
+
+/* tr_reduce whose last step projects the kept tokens instead of copying
+ * them (the step after the path: the kept tokens go through the projector):
+ *   out[k, :] = X[kept row k] . W^T, W device bf16 [Nout, D] (row stride ldw),
+ *   out device bf16 [sum K, Nout]
+ * The kept rows are read from X by the GEMM itself; no gathered copy is made.
+ * Nout must be a multiple of 128 and D of 64.  Other arguments as tr_reduce
+ * (X_pre / X_post may be NULL under the same rule). */
+tr_status tr_reduce_project(tr_ctx* ctx, const void* X, const void* X_pre,
+                            const void* X_post, int32_t B, const int32_t* N,
+                            const int32_t* K, const void* W, int64_t ldw,
+                            int32_t Nout, void* out, int32_t* out_idx,
+                            uint8_t* out_src, void* stream);
+
 /* Host-only budget plan (Algorithm 1, step 1 and the stride of step 6) with
  * the same validation tr_reduce applies; needs no device.  p may carry zero
  * capacities (then only the per-image rules are checked).  For each image

@@ -31,6 +31,7 @@ _LIB = os.path.join(_HERE, "libaltr_oracle.so")
 
 DTYPE_F32 = 0
 DTYPE_BF16 = 1
+DTYPE_F64 = 2
 
 _lib = None
 
@@ -106,8 +107,22 @@ def as_raw(t) -> tuple[np.ndarray, int]:
     if a.dtype == np.uint16:
         return a, DTYPE_BF16
     if a.dtype == np.float64:
-        raise TypeError("oracle rows must be float32 or bfloat16 bit patterns")
+        return a, DTYPE_F64
     raise TypeError("unsupported dtype %s" % a.dtype)
+
+
+def as_f64(t) -> np.ndarray:
+    """The values of float32 / bfloat16 / float64 rows (numpy or CPU torch) as float64, exactly."""
+    a, dt = as_raw(t)
+    if dt == DTYPE_BF16:
+        return (a.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    return a.astype(np.float64)
+
+
+def matmul_bt(A, B) -> np.ndarray:
+    """A . B^T in float64 (numpy) from exactly widened inputs: the linear layers
+    around the path (the encoder MLP's second layer, the projector)."""
+    return as_f64(A) @ as_f64(B).T
 
 
 def renyi2(row) -> float:

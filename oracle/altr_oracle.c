@@ -29,8 +29,9 @@
  *     positions 0, t, 2t, ... counted from 0;
  *   - X* is returned in ascending original token index.
  *
- * Inputs are rows of IEEE binary32 (dtype 0) or bfloat16 (dtype 1, the upper
- * half of a binary32).  Both widen to double exactly.
+ * Inputs are rows of IEEE binary32 (dtype 0), bfloat16 (dtype 1, the upper
+ * half of a binary32) or binary64 (dtype 2, e.g. an exact product computed
+ * in double).  All widen to double exactly.
  *
  * Parity pins: every function here is checked by the CPU test suite against
  * closed forms, invariants, library routines (numpy lexsort) and brute-force
@@ -43,6 +44,7 @@
 
 #define ORACLE_DTYPE_F32 0
 #define ORACLE_DTYPE_BF16 1
+#define ORACLE_DTYPE_F64 2
 
 /* ---- element access --------------------------------------------------- */
 
@@ -57,12 +59,14 @@ static double elem(const void* base, int dtype, size_t i)
         memcpy(&f, &w, sizeof f);
         return (double)f;
     }
+    if (dtype == ORACLE_DTYPE_F64)
+        return ((const double*)base)[i];
     return (double)((const float*)base)[i];
 }
 
 static size_t elem_bytes(int dtype)
 {
-    return dtype == ORACLE_DTYPE_BF16 ? 2u : 4u;
+    return dtype == ORACLE_DTYPE_BF16 ? 2u : dtype == ORACLE_DTYPE_F64 ? 8u : 4u;
 }
 
 /* ---- Stage I: Eq. (3) and Eq. (4) ------------------------------------- */

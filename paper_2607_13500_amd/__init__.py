@@ -179,6 +179,97 @@ class Reducer:
         _check(st, "tr_reduce")
         return ReduceResult(out, out_idx, out_src, h2, s)
 
+    # -- the steps around the path (bf16) ------------------------------------
+    def _check_mat(self, name, t, cols=None):
+        if not isinstance(t, torch.Tensor) or t.device != self.device or t.dtype != torch.bfloat16 \
+                or t.dim() != 2 or t.stride(1) != 1 or (cols is not None and t.shape[1] != cols):
+            raise ValueError("%s must be a bf16 [rows, %s] tensor with unit column stride on %s"
+                             % (name, cols, self.device))
+
+    def gemm(self, A: torch.Tensor, B: torch.Tensor, rows: Optional[torch.Tensor] = None,
+             out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+        """C = A[rows] . B^T (bf16, fp32 accumulation) on the matrix cores.
+
+        A [R, K], B [N, K]; rows (int32 [M], indices into A; out-of-range rows
+        read as zeros) or None for all rows of A.
+        """
+        self._check_mat("A", A)
+        self._check_mat("B", B, A.shape[1])
+        M = A.shape[0] if rows is None else rows.numel()
+        N, K = B.shape
+        if rows is not None and (rows.dtype != torch.int32 or rows.device != self.device
+                                 or not rows.is_contiguous()):
+            raise ValueError("rows must be a contiguous int32 tensor on %s" % self.device)
+        if out is None:
+            out = torch.empty(M, N, dtype=torch.bfloat16, device=self.device)
+        self._check_mat("out", out, N)
+        st = self.lib.tr_gemm_bf16(self._ctx, _ptr(A), A.stride(0), _ptr(rows), A.shape[0], _ptr(B),
+                                   B.stride(0), _ptr(out), out.stride(0), M, N, K, self._stream(stream))
+        _check(st, "tr_gemm_bf16")
+        return out
+
+    def mlp_out_cos(self, Hact: torch.Tensor, W2: torch.Tensor, Xpre: torch.Tensor, *,
+                    out: Optional[torch.Tensor] = None, stream=None):
+        """(X_post, s): X_post = Hact . W2^T with s = cos(X_pre, X_post) fused in."""
+        self._check_mat("Hact", Hact)
+        self._check_mat("W2", W2, Hact.shape[1])
+        self._check_rows("Xpre", Xpre, self.Dc)
+        M, Hd = Hact.shape
+        if W2.shape[0] != self.Dc or Xpre.shape[0] != M:
+            raise ValueError("W2 must be [Dc, Hd] and Xpre [M, Dc]")
+        if out is None:
+            out = torch.empty(M, self.Dc, dtype=torch.bfloat16, device=self.device)
+        self._check_rows("out", out, self.Dc)
+        s = torch.empty(M, dtype=torch.float32, device=self.device)
+        st = self.lib.tr_mlp_out_cos(self._ctx, _ptr(Hact), Hact.stride(0), _ptr(W2), W2.stride(0),
+                                     _ptr(Xpre), _ptr(out), M, Hd, _ptr(s), self._stream(stream))
+        _check(st, "tr_mlp_out_cos")
+        return out, s
+
+    def reduce_given_s(self, X: torch.Tensor, key_s: torch.Tensor, N: Sequence[int],
+                       K: Optional[Sequence[int]] = None, *, out=None, out_idx=None, out_src=None,
+                       want_src: bool = True, stream=None) -> ReduceResult:
+        """The module with the Stage II key supplied (e.g. by mlp_out_cos)."""
+        self._check_rows("X", X, self.D)
+        rows = X.shape[0]
+        if key_s.dtype != torch.float32 or key_s.device != self.device or key_s.numel() != rows \
+                or not key_s.is_contiguous() or sum(int(n) for n in N) != rows:
+            raise ValueError("key_s must be a contiguous float32 [sum N] tensor")
+        sk = sum(self.kept_counts(N, K)) if len(N) else 0
+        dev = self.device
+        out = torch.empty(sk, self.D, dtype=self.dtype, device=dev) if out is None else out
+        out_idx = torch.empty(sk, dtype=torch.int32, device=dev) if out_idx is None else out_idx
+        if out_src is None and want_src:
+            out_src = torch.empty(sk, dtype=torch.uint8, device=dev)
+        st = self.lib.tr_reduce_given_s(self._ctx, _ptr(X), _ptr(key_s), len(N), _i32(N),
+                                        None if K is None else _i32(K), _ptr(out), _ptr(out_idx),
+                                        _ptr(out_src), None, self._stream(stream))
+        _check(st, "tr_reduce_given_s")
+        return ReduceResult(out, out_idx, out_src, None, None)
+
+    def reduce_project(self, X: torch.Tensor, Xpre: Optional[torch.Tensor], Xpost: Optional[torch.Tensor],
+                       N: Sequence[int], K: Optional[Sequence[int]], W: torch.Tensor, *, out=None,
+                       out_idx=None, out_src=None, want_src: bool = True, stream=None) -> ReduceResult:
+        """The module with its gather replaced by the projection X[kept] . W^T (W [Nout, D])."""
+        self._check_rows("X", X, self.D)
+        self._check_mat("W", W, self.D)
+        if (Xpre is None) != (Xpost is None):
+            raise ValueError("Xpre and Xpost must both be given or both be None")
+        if Xpre is not None:
+            self._check_rows("Xpre", Xpre, self.Dc)
+            self._check_rows("Xpost", Xpost, self.Dc)
+        sk = sum(self.kept_counts(N, K)) if len(N) else 0
+        dev, nout = self.device, W.shape[0]
+        out = torch.empty(sk, nout, dtype=torch.bfloat16, device=dev) if out is None else out
+        out_idx = torch.empty(sk, dtype=torch.int32, device=dev) if out_idx is None else out_idx
+        if out_src is None and want_src:
+            out_src = torch.empty(sk, dtype=torch.uint8, device=dev)
+        st = self.lib.tr_reduce_project(self._ctx, _ptr(X), _ptr(Xpre), _ptr(Xpost), len(N), _i32(N),
+                                        None if K is None else _i32(K), _ptr(W), W.stride(0), nout,
+                                        _ptr(out), _ptr(out_idx), _ptr(out_src), self._stream(stream))
+        _check(st, "tr_reduce_project")
+        return ReduceResult(out, out_idx, out_src, None, None)
+
     def score(self, X: Optional[torch.Tensor], Xpre: Optional[torch.Tensor],
               Xpost: Optional[torch.Tensor], *, want_h2: bool = False, out=None, stream=None):
         """Scoring kernel alone: (CV^2 key, s, H2), float32 [rows] each.

@@ -59,6 +59,14 @@ def load(build_if_missing: bool = True) -> ctypes.CDLL:
     lib.tr_score.restype = i32
     lib.tr_select.argtypes = [vp, vp, vp, i32, vp, vp, vp, vp, vp]
     lib.tr_select.restype = i32
+    lib.tr_gemm_bf16.argtypes = [vp, vp, i64, vp, i64, vp, i64, vp, i64, i32, i32, i32, vp]
+    lib.tr_gemm_bf16.restype = i32
+    lib.tr_mlp_out_cos.argtypes = [vp, vp, i64, vp, i64, vp, vp, i32, i32, vp, vp]
+    lib.tr_mlp_out_cos.restype = i32
+    lib.tr_reduce_given_s.argtypes = [vp, vp, vp, i32, vp, vp, vp, vp, vp, vp, vp]
+    lib.tr_reduce_given_s.restype = i32
+    lib.tr_reduce_project.argtypes = [vp, vp, vp, vp, i32, vp, vp, vp, i64, i32, vp, vp, vp, vp]
+    lib.tr_reduce_project.restype = i32
     lib.tr_plan.argtypes = [P(Params), i32, vp, vp, vp, vp, vp, vp]
     lib.tr_plan.restype = i32
     lib.tr_capacity_N.argtypes = []

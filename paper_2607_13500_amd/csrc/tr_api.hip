@@ -185,6 +185,7 @@ struct tr_ctx {
     int32_t* rows = nullptr;
     uint32_t* gsel = nullptr;     // pick bitmaps of images shared by several workgroups
     uint32_t* gimp = nullptr;     // their X^imp bitmaps
+    float* cos_part = nullptr;    // per-tile cosine partials of tr_mlp_out_cos (bf16, Dc % 128 == 0)
     bool timing = false;
     std::vector<hipEvent_t> events;   // 4 per timed call
     int timed = 0;
@@ -331,9 +332,16 @@ tr_status tr_create(const tr_params* p, tr_ctx** out)
         tr_destroy(c);
         return hip_fail(e, "scratch initialisation");
     }
-    if ((e = tr::select_prepare(lds)) != hipSuccess) {
+    if ((e = tr::select_prepare(lds)) != hipSuccess || (e = tr::gemm_prepare()) != hipSuccess) {
         tr_destroy(c);
         return hip_fail(e, "hipFuncSetAttribute");
+    }
+    if (p->dtype == TR_BF16 && c->Dc % 128 == 0) {
+        const size_t words = n * (size_t)tr::gemm_part_cols(c->Dc) * 3;
+        if ((e = hipMalloc(&c->cos_part, words * sizeof(float))) != hipSuccess) {
+            tr_destroy(c);
+            return fail(TR_ENOMEM, "hipMalloc of %zu cosine partials failed", words);
+        }
     }
     *out = c;
     return TR_OK;
@@ -348,6 +356,7 @@ void tr_destroy(tr_ctx* c)
     if (c->rows) (void)hipFree(c->rows);
     if (c->gsel) (void)hipFree(c->gsel);
     if (c->gimp) (void)hipFree(c->gimp);
+    if (c->cos_part) (void)hipFree(c->cos_part);
     for (hipEvent_t ev : c->events) (void)hipEventDestroy(ev);
     delete c;
 }
@@ -396,42 +405,85 @@ tr_status tr_timing_read(tr_ctx* c, double* ms, int64_t* calls)
     return TR_OK;
 }
 
-tr_status tr_reduce(tr_ctx* c, const void* X, const void* X_pre, const void* X_post, int32_t B,
-                    const int32_t* N, const int32_t* K, void* out, int32_t* out_idx,
-                    uint8_t* out_src, float* out_h2, float* out_s, void* stream)
+}  // extern "C"
+
+namespace {
+
+// One call of the module: tr_reduce, or one of its two fused forms (Stage II
+// key supplied; projection of the kept rows instead of their copy).
+struct ReduceCall {
+    const void* X = nullptr;
+    const void* X_pre = nullptr;
+    const void* X_post = nullptr;
+    const float* key_s = nullptr;   // supplied Stage II key, or nullptr
+    int32_t B = 0;
+    const int32_t* N = nullptr;
+    const int32_t* K = nullptr;
+    void* out = nullptr;
+    int32_t* out_idx = nullptr;
+    uint8_t* out_src = nullptr;
+    float* out_h2 = nullptr;
+    float* out_s = nullptr;
+    const void* W = nullptr;        // projector weight [Nout, D], or nullptr: gather
+    int64_t ldw = 0;
+    int32_t Nout = 0;
+    void* stream = nullptr;
+};
+
+tr_status reduce_impl(tr_ctx* c, ReduceCall r)
 {
-    g_err.clear();
     if (!c) return fail(TR_EINVAL, "ctx is NULL");
     Plan pl;
-    tr_status st = check_ctx_plan(c, B, N, K, pl);
+    tr_status st = check_ctx_plan(c, r.B, r.N, r.K, pl);
     if (st != TR_OK) return st;
-    if (B == 0) return TR_OK;
-    if (!X || !out || !out_idx) return fail(TR_EINVAL, "X, out and out_idx must be non-NULL");
+    if (r.B == 0) return TR_OK;
+    if (!r.X || !r.out || !r.out_idx) return fail(TR_EINVAL, "X, out and out_idx must be non-NULL");
     // Which scores the call needs: Stage I's when some image ranks by it or
     // H2 is asked for, Stage II's likewise (lambda = 1 never needs s, lambda
     // = 0 never needs H2).  A score that is not needed is not computed and its
-    // inputs are not read.
-    int mode = (pl.keys_imp || out_h2 ? tr::kScoreImp : 0) | (pl.keys_s || out_s ? tr::kScoreSim : 0);
+    // inputs are not read.  A supplied Stage II key replaces the s score.
+    int mode = (pl.keys_imp || r.out_h2 ? tr::kScoreImp : 0) |
+               (!r.key_s && (pl.keys_s || r.out_s) ? tr::kScoreSim : 0);
     if ((mode & tr::kScoreImp) && (c->p.flags & TR_FLAG_SHANNON)) mode |= tr::kScoreShannon;
     const bool need_c = (mode & tr::kScoreSim) != 0;
-    if (need_c && (!X_pre || !X_post))
+    if (need_c && (!r.X_pre || !r.X_post))
         return fail(TR_EINVAL, "X_pre and X_post must be non-NULL when Stage II ranks tokens or out_s is set");
-    if (!need_c) X_pre = X_post = nullptr;
+    if (!need_c) r.X_pre = r.X_post = nullptr;
     const uintptr_t em = (uintptr_t)c->eb - 1;
-    if (((uintptr_t)X | (uintptr_t)X_pre | (uintptr_t)X_post | (uintptr_t)out) & em)
+    if (((uintptr_t)r.X | (uintptr_t)r.X_pre | (uintptr_t)r.X_post | (uintptr_t)r.out) & em)
         return fail(TR_EINVAL, "tensor base pointers must be aligned to the element size");
-    if (((uintptr_t)out_idx | (uintptr_t)out_h2 | (uintptr_t)out_s) & 3u)
-        return fail(TR_EINVAL, "out_idx, out_h2 and out_s must be 4-byte aligned");
+    if (((uintptr_t)r.out_idx | (uintptr_t)r.out_h2 | (uintptr_t)r.out_s | (uintptr_t)r.key_s) & 3u)
+        return fail(TR_EINVAL, "out_idx, out_h2, out_s and key_s must be 4-byte aligned");
 
     const int64_t row_bytes = (int64_t)c->p.D * c->eb;
     const int64_t rowc_bytes = (int64_t)c->Dc * c->eb;
-    const bool vec_score = aligned16(X) && aligned16(X_pre) && aligned16(X_post) &&
+    const bool vec_score = aligned16(r.X) && aligned16(r.X_pre) && aligned16(r.X_post) &&
                            row_bytes % 16 == 0 && rowc_bytes % 16 == 0;
-    const bool vec_gather = aligned16(X) && aligned16(out) && row_bytes % 16 == 0;
+    const bool vec_gather = aligned16(r.X) && aligned16(r.out) && row_bytes % 16 == 0;
+    tr::GemmArgs ga{};
+    if (r.W) {
+        if (c->p.dtype != TR_BF16) return fail(TR_EUNSUPPORTED, "the projection needs a bf16 context");
+        if (!tr::gemm_shape_ok((int)pl.sum_k, r.Nout, c->p.D))
+            return fail(TR_EUNSUPPORTED, "projection needs Nout %% 128 == 0 and D %% 64 == 0 (Nout = %d, D = %d)",
+                        r.Nout, c->p.D);
+        if (!aligned16(r.X) || row_bytes % 16 || !aligned16(r.W) || (r.ldw * 2) % 16 || r.ldw < c->p.D)
+            return fail(TR_EINVAL, "X, W and their row strides must be 16-byte aligned (ldw >= D)");
+        ga.A = r.X;
+        ga.arows = c->rows;
+        ga.arow_count = pl.sum_n;
+        ga.B = r.W;
+        ga.C = r.out;
+        ga.M = (int32_t)pl.sum_k;
+        ga.N = r.Nout;
+        ga.K = c->p.D;
+        ga.lda = c->p.D;
+        ga.ldb = r.ldw;
+        ga.ldc = r.Nout;
+    }
 
     DeviceGuard g(c->device);
     if (!g.ok) return fail(TR_EDEVICE, "hipSetDevice(%d) failed", c->device);
-    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipStream_t s = static_cast<hipStream_t>(r.stream);
     hipEvent_t* ev = nullptr;
     if (c->timing) {
         if (c->timed < kTimedCalls) ev = &c->events[(size_t)(c->timed++) * 4];
@@ -442,29 +494,171 @@ tr_status tr_reduce(tr_ctx* c, const void* X, const void* X_pre, const void* X_p
 
     if (mode) {
         tr::ScoreArgs sa;
-        sa.X = X;
-        sa.P = X_pre;
-        sa.Q = X_post;
+        sa.X = r.X;
+        sa.P = r.X_pre;
+        sa.Q = r.X_post;
         sa.rows = pl.sum_n;
         sa.D = c->p.D;
         sa.Dc = c->Dc;
         sa.key_imp = c->key_imp;
-        sa.key_s = c->key_s;
-        sa.out_h2 = out_h2;
-        sa.out_s = out_s;
+        sa.key_s = r.key_s ? nullptr : c->key_s;
+        sa.out_h2 = r.out_h2;
+        sa.out_s = r.out_s;
         sa.logD = (float)log((double)c->p.D);
         if ((e = tr::launch_score(sa, c->p.dtype == TR_BF16, vec_score, mode, s)) != hipSuccess)
             return hip_fail(e, "score kernel launch");
     }
     if (ev && (e = hipEventRecord(ev[1], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
 
-    if ((e = run_select(c, pl, c->key_imp, c->key_s, out_idx, out_src, c->rows, s)) != hipSuccess)
+    if ((e = run_select(c, pl, c->key_imp, r.key_s ? r.key_s : c->key_s, r.out_idx, r.out_src, c->rows, s)) !=
+        hipSuccess)
         return hip_fail(e, "select kernel launch");
     if (ev && (e = hipEventRecord(ev[2], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
 
-    if ((e = tr::launch_gather(X, out, c->rows, pl.sum_k, pl.sum_n, row_bytes, c->eb, vec_gather, s)) != hipSuccess)
-        return hip_fail(e, "gather kernel launch");
+    if (r.W) e = tr::launch_gemm(ga, s);
+    else e = tr::launch_gather(r.X, r.out, c->rows, pl.sum_k, pl.sum_n, row_bytes, c->eb, vec_gather, s);
+    if (e != hipSuccess) return hip_fail(e, r.W ? "projection kernel launch" : "gather kernel launch");
     if (ev && (e = hipEventRecord(ev[3], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    return TR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+tr_status tr_reduce(tr_ctx* c, const void* X, const void* X_pre, const void* X_post, int32_t B,
+                    const int32_t* N, const int32_t* K, void* out, int32_t* out_idx,
+                    uint8_t* out_src, float* out_h2, float* out_s, void* stream)
+{
+    g_err.clear();
+    ReduceCall r;
+    r.X = X;
+    r.X_pre = X_pre;
+    r.X_post = X_post;
+    r.B = B;
+    r.N = N;
+    r.K = K;
+    r.out = out;
+    r.out_idx = out_idx;
+    r.out_src = out_src;
+    r.out_h2 = out_h2;
+    r.out_s = out_s;
+    r.stream = stream;
+    return reduce_impl(c, r);
+}
+
+tr_status tr_reduce_given_s(tr_ctx* c, const void* X, const float* key_s, int32_t B, const int32_t* N,
+                            const int32_t* K, void* out, int32_t* out_idx, uint8_t* out_src, float* out_h2,
+                            void* stream)
+{
+    g_err.clear();
+    if (!key_s) return fail(TR_EINVAL, "key_s must be non-NULL");
+    ReduceCall r;
+    r.X = X;
+    r.key_s = key_s;
+    r.B = B;
+    r.N = N;
+    r.K = K;
+    r.out = out;
+    r.out_idx = out_idx;
+    r.out_src = out_src;
+    r.out_h2 = out_h2;
+    r.stream = stream;
+    return reduce_impl(c, r);
+}
+
+tr_status tr_reduce_project(tr_ctx* c, const void* X, const void* X_pre, const void* X_post, int32_t B,
+                            const int32_t* N, const int32_t* K, const void* W, int64_t ldw, int32_t Nout,
+                            void* out, int32_t* out_idx, uint8_t* out_src, void* stream)
+{
+    g_err.clear();
+    if (!W) return fail(TR_EINVAL, "W must be non-NULL");
+    ReduceCall r;
+    r.X = X;
+    r.X_pre = X_pre;
+    r.X_post = X_post;
+    r.B = B;
+    r.N = N;
+    r.K = K;
+    r.W = W;
+    r.ldw = ldw;
+    r.Nout = Nout;
+    r.out = out;
+    r.out_idx = out_idx;
+    r.out_src = out_src;
+    r.stream = stream;
+    return reduce_impl(c, r);
+}
+
+tr_status tr_gemm_bf16(tr_ctx* c, const void* A, int64_t lda, const int32_t* a_rows, int64_t a_row_count,
+                       const void* B, int64_t ldb, void* C, int64_t ldc, int32_t M, int32_t N, int32_t K,
+                       void* stream)
+{
+    g_err.clear();
+    if (!c) return fail(TR_EINVAL, "ctx is NULL");
+    if (M < 0) return fail(TR_EINVAL, "M must be >= 0");
+    if (!tr::gemm_shape_ok(M, N, K))
+        return fail(TR_EUNSUPPORTED, "GEMM needs N %% 128 == 0 and K %% 64 == 0 (N = %d, K = %d)", N, K);
+    if (M == 0) return TR_OK;
+    if (!A || !B || !C) return fail(TR_EINVAL, "A, B and C must be non-NULL");
+    if (!aligned16(A) || !aligned16(B) || (lda * 2) % 16 || (ldb * 2) % 16 || lda < K || ldb < K || ldc < N ||
+        ((uintptr_t)C & 1u) || ((uintptr_t)a_rows & 3u))
+        return fail(TR_EINVAL, "A and B need 16-byte aligned bases and row strides >= K; C stride >= N");
+    if (a_rows && a_row_count < 1) return fail(TR_EINVAL, "a_row_count must be >= 1 with a_rows");
+    DeviceGuard g(c->device);
+    if (!g.ok) return fail(TR_EDEVICE, "hipSetDevice(%d) failed", c->device);
+    tr::GemmArgs ga{};
+    ga.A = A;
+    ga.arows = a_rows;
+    ga.arow_count = a_rows ? a_row_count : M;
+    ga.B = B;
+    ga.C = C;
+    ga.M = M;
+    ga.N = N;
+    ga.K = K;
+    ga.lda = lda;
+    ga.ldb = ldb;
+    ga.ldc = ldc;
+    hipError_t e = tr::launch_gemm(ga, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "GEMM launch");
+    return TR_OK;
+}
+
+tr_status tr_mlp_out_cos(tr_ctx* c, const void* Hact, int64_t ldh, const void* W2, int64_t ldw,
+                         const void* X_pre, void* X_post, int32_t M, int32_t Hd, float* key_s, void* stream)
+{
+    g_err.clear();
+    if (!c) return fail(TR_EINVAL, "ctx is NULL");
+    if (c->p.dtype != TR_BF16) return fail(TR_EUNSUPPORTED, "tr_mlp_out_cos needs a bf16 context");
+    if (!c->cos_part) return fail(TR_EUNSUPPORTED, "tr_mlp_out_cos needs Dc %% 128 == 0 (Dc = %d)", c->Dc);
+    if (M < 0 || (int64_t)M > c->p.max_tokens) return fail(TR_EINVAL, "M must be in [0, max_tokens]");
+    if (!tr::gemm_shape_ok(M, c->Dc, Hd)) return fail(TR_EUNSUPPORTED, "Hd must be a positive multiple of 64");
+    if (M == 0) return TR_OK;
+    if (!Hact || !W2 || !X_pre || !X_post || !key_s)
+        return fail(TR_EINVAL, "Hact, W2, X_pre, X_post and key_s must be non-NULL");
+    if (!aligned16(Hact) || !aligned16(W2) || (ldh * 2) % 16 || (ldw * 2) % 16 || ldh < Hd || ldw < Hd ||
+        ((uintptr_t)X_pre & 1u) || ((uintptr_t)X_post & 1u) || ((uintptr_t)key_s & 3u))
+        return fail(TR_EINVAL, "Hact and W2 need 16-byte aligned bases and row strides >= Hd");
+    DeviceGuard g(c->device);
+    if (!g.ok) return fail(TR_EDEVICE, "hipSetDevice(%d) failed", c->device);
+    tr::GemmArgs ga{};
+    ga.A = Hact;
+    ga.arow_count = M;
+    ga.B = W2;
+    ga.C = X_post;
+    ga.M = M;
+    ga.N = c->Dc;
+    ga.K = Hd;
+    ga.lda = ldh;
+    ga.ldb = ldw;
+    ga.ldc = c->Dc;
+    ga.P = X_pre;
+    ga.ldp = c->Dc;
+    ga.part = c->cos_part;
+    ga.part_cols = tr::gemm_part_cols(c->Dc);
+    ga.s_out = key_s;
+    hipError_t e = tr::launch_gemm(ga, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "GEMM launch");
     return TR_OK;
 }
 

@@ -82,4 +82,25 @@ hipError_t launch_select(const SelectArgs& a, int nmax, hipStream_t s);
 hipError_t launch_gather(const void* X, void* out, const int32_t* rows, int64_t nout, int64_t nrows,
                          int64_t row_bytes, int elem_bytes, bool vec, hipStream_t s);
 
+// ---- bf16 matrix-core GEMM: C[M, N] = A[M, K] . B[N, K]^T -----------------
+struct GemmArgs {
+    const void* A;           // bf16, row m at A + row * lda (16-byte aligned rows)
+    const int32_t* arows;    // [M] row of A for each row of C (gather), or nullptr: row m
+    int64_t arow_count;      // rows of A (gathered indices outside [0, count) read as zeros)
+    const void* B;           // bf16 [N, K], row stride ldb (16-byte aligned rows)
+    void* C;                 // bf16 [M, N], row stride ldc
+    int32_t M, N, K;         // N % 128 == 0, K % 64 == 0
+    int64_t lda, ldb, ldc;   // elements
+    const void* P;           // bf16 [M, N] (stride ldp) for the cosine epilogue, or nullptr
+    int64_t ldp;
+    float* part;             // [M, part_cols, 3] cosine partials (with P)
+    int32_t part_cols;       // N / 128
+    float* s_out;            // [M] cosine of the rows of P and C (with P)
+};
+
+bool gemm_shape_ok(int M, int N, int K);
+int gemm_part_cols(int N);
+hipError_t gemm_prepare();
+hipError_t launch_gemm(const GemmArgs& a, hipStream_t s);
+
 }  // namespace tr

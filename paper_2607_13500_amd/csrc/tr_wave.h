@@ -77,6 +77,20 @@ __device__ __forceinline__ uint32_t wave_or_u32(uint32_t x)
     return (uint32_t)__builtin_amdgcn_readlane((int)wave_scan_or(x), 63);
 }
 
+// Sum over each half of the wavefront: lane 31 ends with the sum of lanes
+// 0-31 and lane 63 with the sum of lanes 32-63 (other lanes hold partial
+// prefixes).  Row shifts inside each row of 16, then lane 15 of rows 0 and 2
+// added into rows 1 and 3.
+__device__ __forceinline__ float half_sum(float x)
+{
+    x += dpp_f32(x, 1);
+    x += dpp_f32(x, 2);
+    x += dpp_f32(x, 4);
+    x += dpp_f32(x, 8);
+    x += dpp_f32(x, 15);
+    return x;
+}
+
 }  // namespace tr
 
 namespace tr {

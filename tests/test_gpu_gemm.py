@@ -1,0 +1,189 @@
+"""GPU parity of the matrix-core GEMM and of the two fusions built on it.
+
+* tr_gemm_bf16 against the oracle's float64 product (oracle.matmul_bt) of the
+  same bf16 inputs: each output is the fp32 sum rounded once to bf16, so
+  |C - C64| <= 2^-8 |C64| + 2 K 2^-24 sum_k |a_k b_k| (rounding to bf16 plus
+  a bound on fp32 accumulation), on ragged M, padded strides and gathered
+  rows (out-of-range indices read as zero rows).
+* tr_mlp_out_cos (Eq. 6 fused into the encoder MLP's second layer): X_post
+  as above and s against the oracle's cosine of x' and the float64 x''
+  within 1e-5 (floor 1), then the whole module with that key against the
+  oracle's selection (parity protocol of tests/parity.py).
+* tr_reduce_project (projection fused with the gather): the kept indices
+  equal tr_reduce's, and the projected rows equal tr_gemm_bf16 applied to
+  tr_reduce's gathered output bit for bit, and the float64 product within the
+  bound above.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import parity
+import synth
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+def say(*a):
+    print("[case]", *a, flush=True)
+    sys.stdout.flush()
+
+
+def reducer(D=4096, Dc=1024, max_tokens=40000, max_images=64, max_N=4096, lam=synth.LAMBDA):
+    import paper_2607_13500_amd as tr
+    return tr.Reducer(D, Dc, torch.bfloat16, lam=lam, max_images=max_images, max_tokens=max_tokens,
+                      max_N=max_N)
+
+
+def randn_bf16(g, *shape, scale=1.0):
+    return (scale * torch.randn(*shape, generator=g)).to(torch.bfloat16)
+
+
+def check_gemm(C, A_rows, B):
+    """C (device bf16) against the float64 product of the given (host) rows."""
+    ref = oracle.matmul_bt(A_rows, B)
+    K = ref.shape[1] and oracle.as_f64(B).shape[1]
+    mag = oracle.matmul_bt(np.abs(oracle.as_f64(A_rows)), np.abs(oracle.as_f64(B)))
+    bound = 2.0 ** -8 * np.abs(ref) + 2 * K * 2.0 ** -24 * mag + 1e-30
+    got = oracle.as_f64(C.cpu())
+    bad = np.abs(got - ref) > bound
+    assert not bad.any(), "%d outputs outside the bound, first at %s" % (bad.sum(), np.argwhere(bad)[:3])
+
+
+@pytest.mark.parametrize("M,N,K,pad", [(1, 128, 64, 0), (300, 256, 128, 0), (257, 384, 512, 8),
+                                       (1000, 1024, 4096, 0), (4096, 4096, 4096, 0)])
+def test_gemm_matches_fp64(M, N, K, pad):
+    say("gemm", M, N, K, "pad", pad)
+    g = torch.Generator().manual_seed(M + N + K)
+    A = randn_bf16(g, M, K + pad)
+    B = randn_bf16(g, N, K + pad)
+    r = reducer()
+    Ad, Bd = A.to(DEV), B.to(DEV)
+    C = r.gemm(Ad[:, :K], Bd[:, :K])
+    torch.cuda.synchronize()
+    check_gemm(C, A[:, :K].contiguous(), B[:, :K].contiguous())
+    r.close()
+
+
+def test_gemm_gathered_rows():
+    say("gemm gather 777 x 384 x 512")
+    g = torch.Generator().manual_seed(3)
+    A = randn_bf16(g, 900, 512)
+    B = randn_bf16(g, 384, 512)
+    rows = torch.randint(-3, 905, (777,), generator=g, dtype=torch.int32)   # duplicates and out-of-range
+    r = reducer()
+    C = r.gemm(A.to(DEV), B.to(DEV), rows=rows.to(DEV))
+    torch.cuda.synchronize()
+    ok = (rows >= 0) & (rows < A.shape[0])
+    Ag = torch.zeros(777, 512, dtype=torch.bfloat16)
+    Ag[ok] = A[rows[ok].long()]
+    check_gemm(C, Ag, B)
+    assert torch.count_nonzero(C[~ok.to(DEV)]) == 0
+    r.close()
+
+
+def test_gemm_rejects_unsupported_shapes():
+    import paper_2607_13500_amd as tr
+    say("gemm shape errors")
+    r = reducer()
+    A = torch.zeros(10, 96, dtype=torch.bfloat16, device=DEV)
+    with pytest.raises(tr.TRError):
+        r.gemm(A, torch.zeros(128, 96, dtype=torch.bfloat16, device=DEV))      # K % 64 != 0
+    with pytest.raises(tr.TRError):
+        r.gemm(A[:, :64], torch.zeros(100, 64, dtype=torch.bfloat16, device=DEV))   # N % 128 != 0
+    r.close()
+
+
+def mlp_inputs(M, Dc, Hd, seed):
+    g = torch.Generator().manual_seed(seed)
+    Xpre = randn_bf16(g, M, Dc)
+    # hidden activations of a GELU-like MLP: mostly positive, some zeros
+    H = torch.relu(torch.randn(M, Hd, generator=g) + 0.3).to(torch.bfloat16)
+    W2 = randn_bf16(g, Dc, Hd, scale=1.0 / np.sqrt(Hd))
+    return Xpre, H, W2
+
+
+@pytest.mark.parametrize("M,Dc,Hd", [(1000, 1024, 4096), (333, 256, 512), (64, 128, 64)])
+def test_mlp_out_cos_parity(M, Dc, Hd):
+    say("mlp_out_cos", M, Dc, Hd)
+    Xpre, H, W2 = mlp_inputs(M, Dc, Hd, M + Dc)
+    Xpre[5] = 0                                                   # zero-norm x': s = 0
+    r = reducer(D=Dc, Dc=Dc, max_tokens=M)
+    Xpost, s = r.mlp_out_cos(H.to(DEV), W2.to(DEV), Xpre.to(DEV))
+    torch.cuda.synchronize()
+    check_gemm(Xpost, H, W2)
+    x64 = oracle.matmul_bt(H, W2)
+    xp = oracle.as_f64(Xpre)
+    s_ref = np.array([oracle.cosine(xp[m], x64[m]) for m in range(M)])
+    sg = s.double().cpu().numpy()
+    err = np.abs(sg - s_ref)
+    print("    max |s - s64| = %.2e" % err.max(), flush=True)
+    assert np.all(err <= parity.TOL * np.maximum(1.0, np.abs(s_ref)))
+    assert sg[5] == 0.0
+    r.close()
+
+
+def test_fused_mlp_module_parity():
+    """Stage II key from the fused epilogue, Stage I from X: the module's
+    selection against the oracle's (H2 of X, cos(x', x'') with x'' exact)."""
+    B, N, D, Dc, Hd, K = 6, 576, 1024, 1024, 4096, 64
+    say("fused mlp module", B, N, D, Dc, Hd, K)
+    w = synth.llava(device="cpu", B=B, N=N, D=D, K=K)
+    Xpre, H, W2 = mlp_inputs(B * N, Dc, Hd, 17)
+    r = reducer(D=D, Dc=Dc, max_tokens=B * N, max_images=B, max_N=N)
+    Xd = w.X.to(DEV)
+    Xpost, s = r.mlp_out_cos(H.to(DEV), W2.to(DEV), Xpre.to(DEV))
+    res = r.reduce_given_s(Xd, s, w.N, w.K)
+    torch.cuda.synchronize()
+    h2, _ = oracle.scores(w.X, w.Xpre, w.Xpost)
+    x64 = oracle.matmul_bt(H, W2)
+    xp = oracle.as_f64(Xpre)
+    s_ref = np.array([oracle.cosine(xp[m], x64[m]) for m in range(B * N)])
+    idx, src = [], []
+    for b in range(B):
+        i, sr = oracle.select(h2[b * N:(b + 1) * N], s_ref[b * N:(b + 1) * N], K, w.lam)
+        idx.append(i)
+        src.append(sr)
+    ref = {"h2": h2, "s": s_ref, "idx": np.concatenate(idx), "src": np.concatenate(src)}
+    wd = synth.Workload(w.name, Xd, None, None, w.N, w.K, w.lam)
+    res = res._replace(s=s)
+    rep = parity.check(wd, res, ref)
+    print("   ", rep.summary(), flush=True)
+    assert rep.ok(), rep.failures[:5]
+    r.close()
+
+
+@pytest.mark.parametrize("name,kw,nout", [("llava", dict(B=8, N=576, D=4096, K=64), 1024),
+                                          ("qwen_ragged", dict(B=3, n_lo=256, n_hi=3000, D=3584), 512)])
+def test_reduce_project_parity(name, kw, nout):
+    say("reduce_project", name, kw, nout)
+    w = synth.make(name, device=DEV, **kw)
+    import paper_2607_13500_amd as tr
+    r = tr.Reducer(w.D, w.Dc, w.dtype, lam=w.lam, max_images=w.B, max_tokens=sum(w.N), max_N=max(w.N))
+    g = torch.Generator().manual_seed(nout)
+    W = randn_bf16(g, nout, w.D, scale=1.0 / np.sqrt(w.D))
+    Wd = W.to(DEV)
+    base = r.reduce(w.X, w.Xpre, w.Xpost, w.N, w.K)
+    proj = r.reduce_project(w.X, w.Xpre, w.Xpost, w.N, w.K, Wd)
+    two_step = r.gemm(base.out, Wd)
+    torch.cuda.synchronize()
+    assert torch.equal(base.idx, proj.idx) and torch.equal(base.src, proj.src)
+    assert torch.equal(proj.out.view(torch.int16), two_step.view(torch.int16))
+    rows = []
+    o0 = r0 = 0
+    idx = proj.idx.cpu().numpy()
+    for n, k in zip(w.N, w.K):
+        rows.append(idx[o0:o0 + k] + r0)
+        o0 += k
+        r0 += n
+    rows = np.concatenate(rows)
+    check_gemm(proj.out, w.X.cpu()[torch.from_numpy(rows).long()], W)
+    # the selection itself against the oracle (the gather path's parity)
+    rep = parity.check(w, base, parity.oracle_reference(w))
+    assert rep.ok(), rep.failures[:5]
+    r.close()

@@ -51,6 +51,8 @@ MUTANTS = [
      "            h2[i] = entropy == 2 ? altr_oracle_shannon(xr, dtype, D)"),
     # bf16 widening
     ("bf16_shift", "        uint32_t w = ((uint32_t)h) << 16;", "        uint32_t w = ((uint32_t)h) << 15;"),
+    ("f64_rows_read_as_f32", "        return ((const double*)base)[i];",
+     "        return (double)((const float*)base)[i];"),
     # the variance form used as a self-check
     ("sample_variance", "    v /= D;", "    v /= (D - 1);"),
     # Eq. (6)

@@ -216,6 +216,33 @@ def test_cosine_closed_forms():
     assert oracle.cosine(RNG.standard_normal(8).astype(np.float32), z) == 0.0
 
 
+def test_cosine_f64_rows():
+    # the same closed forms on float64 rows (the exact product of two bf16
+    # matrices is compared against in float64)
+    for Dc in (1, 3, 1024):
+        x = RNG.standard_normal(Dc)
+        assert oracle.cosine(x, x) == pytest.approx(1.0, abs=1e-14)
+        assert oracle.cosine(x, -3.0 * x) == pytest.approx(-1.0, abs=1e-14)
+        y = RNG.standard_normal(Dc)
+        assert oracle.cosine(x, y) == pytest.approx(float(x @ y / math.sqrt((x @ x) * (y @ y))), rel=1e-12, abs=1e-15)
+    assert oracle.cosine(np.array([3.0, 4.0]), np.array([4.0, 3.0])) == pytest.approx(24 / 25, rel=1e-15)
+    assert oracle.cosine(np.zeros(4), np.ones(4)) == 0.0
+    # float32 rows widened to float64 give the same value
+    x32 = RNG.standard_normal(64).astype(np.float32)
+    y32 = RNG.standard_normal(64).astype(np.float32)
+    assert oracle.cosine(x32.astype(np.float64), y32.astype(np.float64)) == oracle.cosine(x32, y32)
+
+
+def test_matmul_bt_small_integer_brute_force():
+    rng = np.random.default_rng(5)
+    for M, N, K in ((1, 1, 1), (3, 5, 7), (17, 4, 33)):
+        A = rng.integers(-4, 5, (M, K)).astype(np.float32)
+        B = rng.integers(-4, 5, (N, K)).astype(np.float32)
+        want = [[sum(float(A[m, k]) * float(B[n, k]) for k in range(K)) for n in range(N)] for m in range(M)]
+        assert np.array_equal(oracle.matmul_bt(A, B), np.array(want))
+        assert np.array_equal(oracle.matmul_bt(bf16(A), bf16(B)), np.array(want))   # exact in bf16 too
+
+
 def test_scores_batch_matches_single_rows():
     X = RNG.standard_normal((9, 33)).astype(np.float32)
     P = RNG.standard_normal((9, 20)).astype(np.float32)
