@@ -187,3 +187,40 @@ def test_reduce_project_parity(name, kw, nout):
     rep = parity.check(w, base, parity.oracle_reference(w))
     assert rep.ok(), rep.failures[:5]
     r.close()
+
+
+def test_reduce_project_lambda_one_without_states():
+    """lambda = 1 never reads X_pre / X_post, also when the kept rows are projected."""
+    import paper_2607_13500_amd as tr
+    say("reduce_project lambda=1, NULL states")
+    w = synth.llava(device=DEV, B=4, N=576, D=1024, K=64)
+    r = tr.Reducer(w.D, w.Dc, w.dtype, lam=1.0, max_images=w.B, max_tokens=sum(w.N), max_N=576)
+    g = torch.Generator().manual_seed(2)
+    W = randn_bf16(g, 256, w.D, scale=1.0 / np.sqrt(w.D)).to(DEV)
+    a = r.reduce_project(w.X, None, None, w.N, w.K, W)
+    b = r.reduce_project(w.X, w.Xpre, w.Xpost, w.N, w.K, W)
+    torch.cuda.synchronize()
+    assert torch.equal(a.idx, b.idx) and torch.equal(a.out.view(torch.int16), b.out.view(torch.int16))
+    assert int(a.src.sum()) == 0                                   # every kept token from Stage I
+    r.close()
+
+
+def test_mlp_out_cos_rejects_bad_requests():
+    import paper_2607_13500_amd as tr
+    say("mlp_out_cos errors")
+    H = torch.zeros(100, 64, dtype=torch.bfloat16, device=DEV)
+    P = torch.zeros(100, 192, dtype=torch.bfloat16, device=DEV)
+    r = tr.Reducer(192, 192, torch.bfloat16, max_images=1, max_tokens=100, max_N=100)
+    with pytest.raises(tr.TRError):                                # Dc = 192 is not a multiple of 128
+        r.mlp_out_cos(H, torch.zeros(192, 64, dtype=torch.bfloat16, device=DEV), P)
+    r.close()
+    r = tr.Reducer(128, 128, torch.bfloat16, max_images=1, max_tokens=50, max_N=50)
+    with pytest.raises(tr.TRError):                                # M = 100 > max_tokens = 50
+        r.mlp_out_cos(H, torch.zeros(128, 64, dtype=torch.bfloat16, device=DEV),
+                      torch.zeros(100, 128, dtype=torch.bfloat16, device=DEV))
+    r.close()
+    r = tr.Reducer(128, 128, torch.float32, max_images=1, max_tokens=100, max_N=100)
+    with pytest.raises((tr.TRError, ValueError, TypeError)):        # fp32 context
+        r.mlp_out_cos(H, torch.zeros(128, 64, dtype=torch.bfloat16, device=DEV),
+                      torch.zeros(100, 128, dtype=torch.float32, device=DEV))
+    r.close()
