@@ -29,7 +29,7 @@
  * Memory: every pointer named "device" is HIP device memory on the device
  * that was current at tr_create; host arrays are read during the call only.
  * The caller owns all tensors; a context owns only the scratch it allocates
- * in tr_create.  tr_reduce and tr_select allocate nothing.
+ * in tr_create.  No other call allocates memory.
  *
  * Layout: rows are packed back to back.  Image b's rows start at
  * sum_{b' < b} N[b'] in X, X_pre, X_post (and the score outputs), and its
@@ -102,10 +102,14 @@ typedef struct {
 } tr_params;
 
 /* Create a context on the current HIP device: validates p, allocates scratch
- * for max_tokens tokens (12 bytes each) and checks that max_N fits the
- * per-image selection's on-chip memory.  Returns TR_EINVAL for a bad field,
- * TR_EUNSUPPORTED when max_N exceeds the selection capacity (tr_capacity_N),
- * TR_ENOMEM or TR_EDEVICE on runtime failure.  *out is NULL on failure. */
+ * for max_tokens tokens (12 bytes each: two keys and a row index, plus two
+ * bits each for the pick bitmaps of images shared by several workgroups; a
+ * bf16 context with Dc a multiple of 128 also holds 12 x Dc / 128 bytes per
+ * token for tr_mlp_out_cos's per-tile partial sums) and checks that max_N
+ * fits the per-image selection's on-chip memory.  Returns TR_EINVAL for a bad
+ * field, TR_EUNSUPPORTED when max_N exceeds the selection capacity
+ * (tr_capacity_N), TR_ENOMEM or TR_EDEVICE on runtime failure.  *out is NULL
+ * on failure. */
 tr_status tr_create(const tr_params* p, tr_ctx** out);
 
 /* The whole module (steps 1-7 above) on a packed batch of B images.
