@@ -284,6 +284,50 @@ def test_capacity_and_max_n():
         run_and_check(w)
 
 
+# ------------------------------------------------------ non-finite inputs
+
+@pytest.mark.parametrize("N,dtype", [(600, torch.bfloat16), (5000, torch.bfloat16), (300, torch.float32)])
+def test_non_finite_inputs_give_well_formed_output(N, dtype):
+    """NaN and infinite inputs make the scores unspecified, but the selection
+    falls back to its integer paths (a non-finite key range is never
+    bucketed), so the output is still K distinct ascending in-range indices
+    with the stage split of Algorithm 1, and out is the gathered rows."""
+    say("non-finite inputs", N, dtype)
+    g = torch.Generator().manual_seed(N)
+    D = Dc = 256
+    X = torch.randn(N, D, generator=g)
+    P = torch.randn(N, Dc, generator=g)
+    Q = torch.randn(N, Dc, generator=g)
+    X[3, 5] = float("nan")
+    X[7] = float("inf")
+    X[11, :10] = float("-inf")
+    X[13] = float("nan")
+    P[17, 0] = float("nan")
+    Q[19] = float("inf")
+    P[23] = 3.0e38
+    cast = lambda t: t.to(dtype).to(DEV).contiguous()
+    K = N // 7
+    w = synth.Workload("nonfinite", cast(X), cast(P), cast(Q), [N], [K], synth.LAMBDA)
+    r = reducer_for(w)
+    res = r.reduce(w.X, w.Xpre, w.Xpost, w.N, w.K, want_scores=True)
+    # NaN keys straight into the selection
+    ki = torch.randn(N, generator=g)
+    ki[::9] = float("nan")
+    ks = torch.randn(N, generator=g)
+    ks[::5] = float("-inf")
+    ks[1::11] = float("nan")
+    idx2, src2 = r.select(ki.to(DEV), ks.to(DEV), [N], [K])
+    torch.cuda.synchronize()
+    K1, K2, _ = oracle.budget(N, K, synth.LAMBDA)
+    for idx, src in ((res.idx.cpu().numpy(), res.src.cpu().numpy()), (idx2.cpu().numpy(), src2.cpu().numpy())):
+        assert idx.size == K and np.all(np.diff(idx) > 0) and idx.min() >= 0 and idx.max() < N
+        assert int((src == 0).sum()) == K1 and int((src == 1).sum()) == K2
+    rows = res.idx.long()
+    assert torch.equal(res.out.view(torch.int16 if dtype == torch.bfloat16 else torch.int32),
+                       w.X.index_select(0, rows).view(torch.int16 if dtype == torch.bfloat16 else torch.int32))
+    r.close()
+
+
 # ------------------------------------------------------ stream ordering
 
 ORDER_CASES = [
