@@ -547,3 +547,26 @@ def test_shannon_parity_full(name, kw, ratio):
     assert rep.ok(), rep.failures[:5]
     assert rep.stage1_swaps <= max(2, rep.images // 10)
     r.close()
+
+
+FULL_VARIANTS = [("lambda0", dict(lam=0.0)), ("lambda1", dict(lam=1.0)), ("stride_real", dict(stride_real=True))]
+
+
+@pytest.mark.parametrize("name,opt", FULL_VARIANTS, ids=[n for n, _ in FULL_VARIANTS])
+def test_variants_parity_full_llava(name, opt):
+    """The variants at the benchmark size (64 x 576 x 4096 bf16 -> 64), in the
+    launch configuration bench.py times for them."""
+    say("full variant", name)
+    w = synth.llava(device=DEV, B=64, N=576, D=4096, K=64)
+    stride_real = opt.get("stride_real", False)
+    if "lam" in opt:
+        w.lam = opt["lam"]
+    r = reducer_for(w, stride_real=stride_real)
+    states = (None, None) if w.lam == 1.0 else (w.Xpre, w.Xpost)
+    res = r.reduce(w.X, *states, w.N, w.K)
+    ref = parity.oracle_reference(w, stride_mode=1 if stride_real else 0)
+    rep = parity.check(w, res, ref, stride_mode=1 if stride_real else 0)
+    print("   ", name, rep.summary(), flush=True)
+    assert rep.ok(), rep.failures[:5]
+    assert rep.stage1_swaps <= 2 and rep.stage2_near <= max(4, rep.picks // 100)
+    r.close()
