@@ -182,8 +182,9 @@ tr_status tr_select(tr_ctx* ctx, const float* key_imp, const float* key_s,
  *          outside [0, a_row_count) read as zeros (memory-safe)
  *   B      device bf16 [N, K] (row stride ldb), e.g. a Linear layer's weight
  *   C      device bf16 [M, N] (row stride ldc)
- * N must be a multiple of 128 and K of 64 (else TR_EUNSUPPORTED); A and B
- * bases and row strides must be 16-byte aligned (else TR_EINVAL). */
+ * N must be a multiple of 128 and K of 64, and ceil(M / 256) * N / 128 must
+ * stay below 2^31 (else TR_EUNSUPPORTED); A and B bases and row strides must
+ * be 16-byte aligned (else TR_EINVAL). */
 tr_status tr_gemm_bf16(tr_ctx* ctx, const void* A, int64_t lda,
                        const int32_t* a_rows, int64_t a_row_count,
                        const void* B, int64_t ldb, void* C, int64_t ldc,

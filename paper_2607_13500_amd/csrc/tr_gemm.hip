@@ -234,7 +234,10 @@ int gemm_part_cols(int N) { return N / kBN; }
 
 bool gemm_shape_ok(int M, int N, int K)
 {
-    return M >= 0 && N > 0 && K > 0 && N % kBN == 0 && K % kBK == 0;
+    if (M < 0 || N <= 0 || K <= 0 || N % kBN || K % kBK) return false;
+    // output tiles (and the grid, rounded up to the XCD count) fit an int
+    const int64_t tiles = (int64_t)((M + (int64_t)kBM - 1) / kBM) * (N / kBN);
+    return tiles <= (int64_t)INT32_MAX - kXcds;
 }
 
 hipError_t gemm_prepare()

@@ -155,3 +155,14 @@ def test_null_context_calls_are_rejected():
     assert lib.tr_select(None, None, None, 1, N, None, None, None, None) == _lib.TR_EINVAL
     assert lib.tr_score(None, None, None, None, 1, None, None, None, None) == _lib.TR_EINVAL
     lib.tr_destroy(None)
+
+
+def test_gemm_and_fused_entry_points_validate_before_touching_a_device():
+    """Argument errors of the GEMM entry points come back synchronously (no context needed)."""
+    lib = _lib.load()
+    assert lib.tr_gemm_bf16(None, None, 64, None, 0, None, 64, None, 128, 1, 128, 64, None) == _lib.TR_EINVAL
+    assert lib.tr_mlp_out_cos(None, None, 64, None, 64, None, None, 1, 64, None, None) == _lib.TR_EINVAL
+    N = (ctypes.c_int32 * 1)(4)
+    assert lib.tr_reduce_given_s(None, None, None, 1, N, None, None, None, None, None, None) == _lib.TR_EINVAL
+    assert lib.tr_reduce_project(None, None, None, None, 1, N, None, None, 64, 128, None, None, None, None) == _lib.TR_EINVAL
+    assert lib.tr_last_error() != b""
