@@ -64,8 +64,10 @@ def parse():
 
 
 def score_source_sha() -> str:
+    """sha256 of the scoring kernel's sources: the kernel, its interface header
+    and the wavefront helpers it uses."""
     h = hashlib.sha256()
-    for f in ("tr_score.hip", "tr_internal.h"):
+    for f in ("tr_score.hip", "tr_score.h", "tr_wave.h"):
         with open(os.path.join(ROOT, "paper_2607_13500_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()
@@ -96,26 +98,63 @@ def describe(w) -> str:
     return "%s, %d x %s tokens x %d %s -> %s kept" % (kind, w.B, ns, w.D, dt, ks)
 
 
-def cpu_baseline(w, seconds: float, entropy: int = 2, stride_mode: int = 0):
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown CPU"
+
+
+def cpu_baseline(w, seconds: float, entropy: int = 2, stride_mode: int = 0, threads: int = 1):
+    """The fp64 C oracle, unchanged, on a bounded sample of the workload: the
+    first images up to ~40k tokens, repeated to ~`seconds`.  With threads > 1
+    the sample's images are split among that many threads (the oracle runs in
+    C outside Python's lock)."""
+    import concurrent.futures
     import oracle
-    # a bounded sample: the first images up to ~40k tokens, repeated to ~`seconds`
     nb, rows = 0, 0
     while nb < w.B and (nb == 0 or rows + w.N[nb] <= 40000):
         rows += w.N[nb]
         nb += 1
     X, P, Q = w.X[:rows].cpu(), w.Xpre[:rows].cpu(), w.Xpost[:rows].cpu()
+    # image subsets for the threads: contiguous runs of images, about equal rows
+    threads = max(1, min(threads, nb))
+    offs = [0]
+    for n in w.N[:nb]:
+        offs.append(offs[-1] + n)
+    cuts = [0]
+    for t in range(1, threads):
+        target = rows * t / threads
+        b = cuts[-1] + 1
+        while b < nb and offs[b] < target:
+            b += 1
+        cuts.append(min(b, nb))
+    cuts.append(nb)
+    parts = [(cuts[t], cuts[t + 1]) for t in range(threads) if cuts[t] < cuts[t + 1]]
+
+    def run(part):
+        b0, b1 = part
+        oracle.reduce(X[offs[b0]:offs[b1]], P[offs[b0]:offs[b1]], Q[offs[b0]:offs[b1]], w.N[b0:b1],
+                      w.K[b0:b1], w.lam, want_out=True, want_scores=False, entropy=entropy,
+                      stride_mode=stride_mode)
+
     runs = 0
-    t0 = time.perf_counter()
-    while True:
-        oracle.reduce(X, P, Q, w.N[:nb], w.K[:nb], w.lam, want_out=True, want_scores=False,
-                      entropy=entropy, stride_mode=stride_mode)
-        runs += 1
-        el = time.perf_counter() - t0
-        if el >= seconds or runs >= 50:
-            break
-    return {"value": runs * nb / el, "unit": "images/s", "cores": 1, "kind": "oracle",
-            "sample": "%d x the first %d of %d images (%d tokens; fp64 C oracle, one thread, %.1f s)"
-                      % (runs, nb, w.B, rows, el)}
+    with concurrent.futures.ThreadPoolExecutor(max_workers=len(parts)) as ex:
+        t0 = time.perf_counter()
+        while True:
+            list(ex.map(run, parts))
+            runs += 1
+            el = time.perf_counter() - t0
+            if el >= seconds or runs >= 50:
+                break
+    return {"value": runs * nb / el, "unit": "images/s", "cores": len(parts), "kind": "oracle",
+            "sample": "%d x the first %d of %d images (%d tokens; fp64 C oracle, %d thread%s, %.1f s; "
+                      "host: %s, %d logical CPUs)" % (runs, nb, w.B, rows, len(parts),
+                                                      "" if len(parts) == 1 else "s", el, cpu_model(),
+                                                      os.cpu_count() or 0)}
 
 
 def time_steps(torch, f, steps, warmup):
@@ -308,6 +347,25 @@ def main():
     torch.cuda.synchronize()
     score_ms = ev0.elapsed_time(ev1) / args.steps
 
+    # Streaming-read ceiling: the same three tensors read once by a kernel that
+    # does nothing else (16-byte non-temporal loads), timed like the roofline.
+    read_bufs = [t for t in (xs, *states) if t is not None]
+    read_s = time_events(torch, lambda: tr.read_bandwidth(read_bufs), args.steps, stream)
+    read_bytes = sum(t.numel() * t.element_size() for t in read_bufs)
+
+    # Diagnostic: the distribution of single-step times, HIP events around each
+    # step (the events add a little to each step).
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(min(args.steps, 100))]
+    torch.cuda.synchronize()
+    for e0, e1 in evs:
+        e0.record(stream)
+        step()
+        e1.record(stream)
+    torch.cuda.synchronize()
+    step_ev = sorted(e0.elapsed_time(e1) for e0, e1 in evs)
+    pick = lambda q: step_ev[min(len(step_ev) - 1, int(q * len(step_ev)))]
+
     # Diagnostic: per-stage time with HIP events around each kernel of a step
     # (the events themselves add a few microseconds per stage).
     r.timing(True)
@@ -353,17 +411,23 @@ def main():
         "path_hbm": {"algorithmic_bytes": path_bytes,
                      "achieved_GBs": round(path_bytes / (ms_step * 1e-3) / 1e9, 1),
                      "frac": round(path_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
+        "step_ms_events": {"median": round(pick(0.5), 5), "p10": round(pick(0.1), 5),
+                           "p90": round(pick(0.9), 5), "steps": len(step_ev)},
         "stage_ms_with_events": {"score": round(stage_ms[0] / max(calls, 1), 5),
                                  "select": round(stage_ms[1] / max(calls, 1), 5),
                                  "gather": round(stage_ms[2] / max(calls, 1), 5)},
         "roofline": {"kernel": "score_kernel", "bound": "hbm", "achieved": round(achieved, 1),
                      "avg_launch_ms": round(score_ms, 5),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": traffic, "algorithmic_bytes_per_launch": score_bytes},
+                     "traffic": traffic, "algorithmic_bytes_per_launch": score_bytes,
+                     "read_ceiling_GBs": round(read_bytes / read_s / 1e9, 1),
+                     "frac_of_read_ceiling": round(achieved / (read_bytes / read_s / 1e9), 4)},
     }
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds, 1 if args.shannon else 2,
-                                            1 if args.stride_real else 0)
+        ent, sm = (1 if args.shannon else 2), (1 if args.stride_real else 0)
+        line["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds, ent, sm)
+        line["cpu_baseline_all_cores"] = cpu_baseline(w, args.cpu_seconds / 2, ent, sm,
+                                                      threads=min(os.cpu_count() or 1, 16))
     r.close()
     print(json.dumps(line), flush=True)
     if args.calib_copy_mib > 0:

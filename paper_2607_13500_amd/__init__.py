@@ -71,6 +71,18 @@ def plan(N: Sequence[int], K: Optional[Sequence[int]] = None, lam: float = LAMBD
     return tuple([list(o[:B]) for o in outs])
 
 
+def read_bandwidth(buffers, stream=None) -> None:
+    """Measurement hook: read each (16-byte aligned, contiguous) device tensor
+    once with the streaming-read kernel (the read ceiling of the device)."""
+    lib = _lib.load()
+    sink = torch.empty(4096, dtype=torch.int32, device=buffers[0].device)
+    st = stream if stream is not None else torch.cuda.current_stream(buffers[0].device)
+    for b in buffers:
+        nbytes = b.numel() * b.element_size()
+        _check(lib.tr_read_bandwidth(_ptr(b), nbytes - nbytes % 16, _ptr(sink), sink.numel(),
+                                     ctypes.c_void_p(st.cuda_stream)), "tr_read_bandwidth")
+
+
 def capacity_N() -> int:
     """Largest per-image N the selection handles on the current device."""
     return int(_lib.load().tr_capacity_N())

@@ -662,6 +662,18 @@ tr_status tr_mlp_out_cos(tr_ctx* c, const void* Hact, int64_t ldh, const void* W
     return TR_OK;
 }
 
+tr_status tr_read_bandwidth(const void* p, int64_t bytes, uint32_t* sink, int32_t sink_words, void* stream)
+{
+    g_err.clear();
+    if (bytes < 0 || bytes % 16) return fail(TR_EINVAL, "bytes must be a non-negative multiple of 16");
+    if (bytes == 0) return TR_OK;
+    if (!p || !aligned16(p) || !sink || sink_words < 1 || ((uintptr_t)sink & 3u))
+        return fail(TR_EINVAL, "p must be 16-byte aligned, sink a 4-byte aligned buffer of >= 1 word");
+    hipError_t e = tr::launch_read(p, bytes, sink, sink_words, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "read kernel launch");
+    return TR_OK;
+}
+
 tr_status tr_score(tr_ctx* c, const void* X, const void* X_pre, const void* X_post, int64_t rows,
                    float* key_imp, float* key_s, float* out_h2, void* stream)
 {

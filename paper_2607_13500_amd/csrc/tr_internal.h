@@ -6,36 +6,9 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "tr_score.h"
+
 namespace tr {
-
-constexpr int kWave = 64;
-
-// ---- scoring (Eq. 3-4 and Eq. 6, one wavefront per token row) -------------
-struct ScoreArgs {
-    const void* X;       // [rows, D]
-    const void* P;       // [rows, Dc] pre-MLP states
-    const void* Q;       // [rows, Dc] post-MLP states
-    int64_t rows;
-    int32_t D;
-    int32_t Dc;
-    float* key_imp;      // [rows] CV^2 of |x| (Shannon: log D - H1) (Stage I key, ascending), or nullptr
-    float* key_s;        // [rows] s (Stage II key, ascending), or nullptr
-    float* out_h2;       // [rows] H2 (Shannon: H1), or nullptr
-    float* out_s;        // [rows] or nullptr
-    float logD;          // log(D) in fp32
-};
-
-// Which scores a launch computes (a bit set, never 0).  A score left out
-// reads nothing: its key (if the pointer is set) is written as 0, and its
-// optional output is not written.
-constexpr int kScoreImp = 1;   // Eq. (3)-(4) from X: key_imp, out_h2
-constexpr int kScoreSim = 2;   // Eq. (6) from X_pre, X_post: key_s, out_s
-constexpr int kScoreShannon = 4;   // with kScoreImp: Shannon variant (key KL = log D - H1, out H1)
-
-// bf16: true for bfloat16 rows, false for fp32.  vec: every row start is
-// 16-byte aligned (vector loads); otherwise element loads with the same
-// per-lane arithmetic order.
-hipError_t launch_score(const ScoreArgs& a, bool bf16, bool vec, int mode, hipStream_t s);
 
 // ---- per-image selection (top-K1, ordered remainder, sort, stride) --------
 struct ImageDesc {
@@ -81,6 +54,11 @@ hipError_t launch_select(const SelectArgs& a, int nmax, hipStream_t s);
 // rows[r] outside [0, nrows) are skipped (their output row is left as is).
 hipError_t launch_gather(const void* X, void* out, const int32_t* rows, int64_t nout, int64_t nrows,
                          int64_t row_bytes, int elem_bytes, bool vec, hipStream_t s);
+
+// ---- measurement: streaming-read ceiling --------------------------------------
+// Reads bytes / 16 chunks of p (16-byte aligned) once; at most sink_words
+// workgroups, each of which may write sink[its index].
+hipError_t launch_read(const void* p, int64_t bytes, uint32_t* sink, int sink_words, hipStream_t s);
 
 // ---- bf16 matrix-core GEMM: C[M, N] = A[M, K] . B[N, K]^T -----------------
 struct GemmArgs {

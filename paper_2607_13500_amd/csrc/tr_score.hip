@@ -38,7 +38,7 @@
 // refer to the same effective shift 1 / (1/c) and e keeps full relative
 // accuracy for near-uniform rows.  A row whose probe mean is 0 uses the plain
 // form H1 = log S - (sum |x| log |x|) / S instead.
-#include "tr_internal.h"
+#include "tr_score.h"
 #include "tr_wave.h"
 
 namespace tr {

@@ -166,3 +166,18 @@ def test_gemm_and_fused_entry_points_validate_before_touching_a_device():
     assert lib.tr_reduce_given_s(None, None, None, 1, N, None, None, None, None, None, None) == _lib.TR_EINVAL
     assert lib.tr_reduce_project(None, None, None, None, 1, N, None, None, 64, 128, None, None, None, None) == _lib.TR_EINVAL
     assert lib.tr_last_error() != b""
+
+
+def test_read_bandwidth_validates_before_touching_a_device():
+    """The read hook rejects sizes and pointers it cannot stream, and reads
+    nothing for 0 bytes, all without a device call."""
+    lib = _lib.load()
+    sink = ctypes.c_void_p(64)   # never dereferenced: every call below returns first
+    assert lib.tr_read_bandwidth(None, 0, None, 0, None) == _lib.TR_OK
+    assert lib.tr_read_bandwidth(None, -16, sink, 1, None) == _lib.TR_EINVAL
+    assert lib.tr_read_bandwidth(ctypes.c_void_p(256), 24, sink, 1, None) == _lib.TR_EINVAL
+    assert lib.tr_read_bandwidth(None, 16, sink, 1, None) == _lib.TR_EINVAL
+    assert lib.tr_read_bandwidth(ctypes.c_void_p(264), 16, sink, 1, None) == _lib.TR_EINVAL
+    assert lib.tr_read_bandwidth(ctypes.c_void_p(256), 16, sink, 0, None) == _lib.TR_EINVAL
+    assert lib.tr_read_bandwidth(ctypes.c_void_p(256), 16, ctypes.c_void_p(66), 1, None) == _lib.TR_EINVAL
+    assert b"16" in lib.tr_last_error()

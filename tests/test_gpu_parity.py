@@ -570,3 +570,18 @@ def test_variants_parity_full_llava(name, opt):
     assert rep.ok(), rep.failures[:5]
     assert rep.stage1_swaps <= 2 and rep.stage2_near <= max(4, rep.picks // 100)
     r.close()
+
+
+def test_read_bandwidth_hook():
+    import paper_2607_13500_amd as tr
+    from paper_2607_13500_amd import _lib
+    say("read bandwidth hook")
+    buf = torch.ones(1 << 20, dtype=torch.float32, device=DEV)
+    tr.read_bandwidth([buf, buf[: (1 << 19)]])
+    torch.cuda.synchronize()
+    lib = _lib.load()
+    sink = torch.empty(16, dtype=torch.int32, device=DEV)
+    assert lib.tr_read_bandwidth(buf.data_ptr(), 100, sink.data_ptr(), 16, None) == _lib.TR_EINVAL   # not a multiple of 16
+    assert lib.tr_read_bandwidth(buf.data_ptr() + 4, 64, sink.data_ptr(), 16, None) == _lib.TR_EINVAL   # misaligned
+    assert lib.tr_read_bandwidth(buf.data_ptr(), 64, sink.data_ptr(), 0, None) == _lib.TR_EINVAL   # no sink
+    assert lib.tr_read_bandwidth(buf.data_ptr(), 0, None, 0, None) == _lib.TR_OK                  # nothing to read
