@@ -110,7 +110,7 @@ def cpu_model() -> str:
 
 def cpu_baseline(w, seconds: float, entropy: int = 2, stride_mode: int = 0, threads: int = 1):
     """The fp64 C oracle, unchanged, on a bounded sample of the workload: the
-    first images up to ~40k tokens, repeated to ~`seconds`.  With threads > 1
+    first images up to ~40k tokens, repeated to ~`seconds` in three trials.  With threads > 1
     the sample's images are split among that many threads (the oracle runs in
     C outside Python's lock)."""
     import concurrent.futures
@@ -141,20 +141,27 @@ def cpu_baseline(w, seconds: float, entropy: int = 2, stride_mode: int = 0, thre
                       w.K[b0:b1], w.lam, want_out=True, want_scores=False, entropy=entropy,
                       stride_mode=stride_mode)
 
-    runs = 0
+    # three timed trials of about seconds / 3 each; the value is their median
+    rates, reps, total = [], 0, 0.0
     with concurrent.futures.ThreadPoolExecutor(max_workers=len(parts)) as ex:
-        t0 = time.perf_counter()
-        while True:
-            list(ex.map(run, parts))
-            runs += 1
-            el = time.perf_counter() - t0
-            if el >= seconds or runs >= 50:
-                break
-    return {"value": runs * nb / el, "unit": "images/s", "cores": len(parts), "kind": "oracle",
-            "sample": "%d x the first %d of %d images (%d tokens; fp64 C oracle, %d thread%s, %.1f s; "
-                      "host: %s, %d logical CPUs)" % (runs, nb, w.B, rows, len(parts),
-                                                      "" if len(parts) == 1 else "s", el, cpu_model(),
-                                                      os.cpu_count() or 0)}
+        for _ in range(3):
+            runs = 0
+            t0 = time.perf_counter()
+            while True:
+                list(ex.map(run, parts))
+                runs += 1
+                el = time.perf_counter() - t0
+                if el >= seconds / 3 or runs >= 500:
+                    break
+            rates.append(runs * nb / el)
+            reps += runs
+            total += el
+    return {"value": sorted(rates)[1], "unit": "images/s", "cores": len(parts), "kind": "oracle",
+            "trials_images_per_s": [round(r, 1) for r in rates],
+            "sample": "median of 3 trials, %d repetitions in all of the first %d of %d images (%d tokens; "
+                      "fp64 C oracle, %d thread%s, %.1f s; host: %s, %d logical CPUs)"
+                      % (reps, nb, w.B, rows, len(parts), "" if len(parts) == 1 else "s", total,
+                         cpu_model(), os.cpu_count() or 0)}
 
 
 def time_steps(torch, f, steps, warmup):
@@ -223,7 +230,7 @@ def bench_fused(args, torch, synth, tr, dev):
                        "images": w.B, "tokens": rows, "D": w.D, "Dc": Dc, "hidden": Hd},
             "unfused": {"ms_per_step": round(t_u * 1e3, 5), "value": round(w.B / t_u, 1),
                         "what": "library GEMM (torch.matmul) + tr_reduce reading X_pre and X_post"},
-            "roofline": {"kernel": "gemm_kernel<cos epilogue> + cos_finish", "bound": "mfma",
+            "roofline": {"kernel": "gemm_wide_kernel<cos epilogue> + cos_finish", "bound": "mfma",
                          "achieved": round(flops / t_gemm / 1e12, 1), "avg_launch_ms": round(t_gemm * 1e3, 5),
                          "peak": 2500.0, "unit": "TFLOP/s", "frac": round(flops / t_gemm / 1e12 / 2500.0, 4),
                          "traffic": None, "algorithmic_flops_per_launch": flops,
@@ -264,7 +271,7 @@ def bench_fused(args, torch, synth, tr, dev):
                        "images": w.B, "tokens": rows, "D": w.D, "kept": sk, "Nout": nout},
             "unfused": {"ms_per_step": round(t_u * 1e3, 5), "value": round(w.B / t_u, 1),
                         "what": "tr_reduce (gathered copy) + library GEMM (torch.matmul)"},
-            "roofline": {"kernel": "gemm_kernel<row gather>", "bound": "mfma",
+            "roofline": {"kernel": "gemm_wide_kernel<row gather>", "bound": "mfma",
                          "achieved": round(flops / t_gemm / 1e12, 1), "avg_launch_ms": round(t_gemm * 1e3, 5),
                          "peak": 2500.0, "unit": "TFLOP/s", "frac": round(flops / t_gemm / 1e12 / 2500.0, 4),
                          "traffic": None, "algorithmic_flops_per_launch": flops,

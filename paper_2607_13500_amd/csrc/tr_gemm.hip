@@ -10,16 +10,26 @@
 //     hidden activations) and P = x' its input, these are Eq. (6)'s three sums,
 //     so the Stage II score needs no further pass over X_pre or X_post.
 //
-// Tiling for gfx950 (64-wide wavefronts, 32x32x16 bf16 MFMA):
-//   * workgroup tile 256 x 128 x 64, four wavefronts in a 2 x 2 grid, each
-//     owning 128 x 64 of C as 4 x 2 MFMA tiles (128 fp32 accumulators a lane);
-//   * one LDS stage holding the A and B k-tiles, rows padded from 128 to 144
-//     bytes so that the 16-byte fragment reads of a wavefront hit distinct
-//     banks; the next k-tile is prefetched into registers while the current
-//     one feeds the MFMAs (54 KB of LDS: two workgroups fit a CU);
-//   * XCD-aware tile order: workgroup b runs on XCD b % 8; each XCD takes a
-//     contiguous run of output tiles with the N tile fastest, so the
-//     workgroups sharing an A block-row share that XCD's L2.
+// Two tilings for gfx950 (64-wide wavefronts, 32x32x16 bf16 MFMA), both with
+// the same per-element MFMA sequence (k ascending in steps of 16), so they give
+// bit-identical C:
+//   * wide (N % 256 == 0, K % 128 == 0): workgroup tile 256 x 256 x 64, eight
+//     wavefronts in a 2 x 4 grid, each owning 128 x 64 of C (128 fp32
+//     accumulators a lane).
+//     Operands go from global memory straight into LDS (buffer loads with the
+//     LDS-destination form, 16 bytes a lane), two LDS stages of 64 KB, so the
+//     next k-tile streams in while the current one feeds the MFMAs with no
+//     staging registers.  LDS rows are 128 bytes with the 16-byte chunks
+//     XOR-swizzled by (row / 2) % 8, which keeps the fragment reads of any 16
+//     consecutive rows on distinct banks.  Buffer range checking reads rows
+//     past the end of A (or invalid gathered rows) as zeros.
+//   * narrow (every other shape, or operands beyond 31-bit buffer offsets):
+//     workgroup tile 256 x 128 x 64, four wavefronts of 128 x 64, rows padded
+//     from 128 to 144 bytes for conflict-free fragment reads, the next k-tile
+//     prefetched into registers (54 KB of LDS: two workgroups fit a CU).
+// Both use an XCD-aware tile order: workgroup b runs on XCD b % 8; each XCD
+// takes a contiguous run of output tiles with the N tile fastest, so the
+// workgroups sharing an A block-row share that XCD's L2.
 //
 // MFMA operand layout (32x32x16 bf16, verified on the device): lane l holds
 // A row l % 32 and B column l % 32, k = (l / 32) * 8 .. + 8; accumulator
@@ -210,13 +220,223 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmArgs a)
     }
 }
 
+// ---- wide tiling -----------------------------------------------------------
+constexpr int kWBN = 256;
+constexpr int kWThreads = 512;
+constexpr int kWStage = kBM * kBK * 2;              // one operand k-tile: 256 rows x 128 B
+constexpr int kWRed = 4 * kBM * 3;                  // cosine partials of the four N-quarters (floats)
+constexpr uint32_t kBufWord3 = 0x00020000u;        // raw buffer resource, 32-bit elements
+constexpr uint32_t kBadRow = 0x80000000u;          // a buffer offset past every resource
+
+typedef __attribute__((address_space(3))) unsigned char lds_t;
+typedef __attribute__((address_space(3))) bf16x8 lds_frag;
+typedef __attribute__((address_space(3))) void lds_void;
+
+template <bool GATHER, bool COS>
+__global__ __launch_bounds__(kWThreads, 1) void gemm_wide_kernel(GemmArgs a)
+{
+    __shared__ __attribute__((aligned(1024))) unsigned char sA0[kWStage], sA1[kWStage], sB0[kWStage], sB1[kWStage];
+    __shared__ float red[COS ? kWRed : 1];
+    lds_t* const a0 = (lds_t*)sA0;
+    lds_t* const a1 = (lds_t*)sA1;
+    lds_t* const b0 = (lds_t*)sB0;
+    lds_t* const b1 = (lds_t*)sB1;
+
+    const int mt = (a.M + kBM - 1) / kBM, nt = a.N / kWBN;
+    const int tiles = mt * nt;
+    const int per_xcd = (tiles + kXcds - 1) / kXcds;
+    const int t = (int)(blockIdx.x % kXcds) * per_xcd + (int)(blockIdx.x / kXcds);
+    if (t >= tiles) return;   // whole workgroup leaves together
+    const int m0 = (t / nt) * kBM, n0 = (t % nt) * kWBN;
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = w >> 2, wn = w & 3;   // 2 x 4 wavefront grid
+
+    // ---- global -> LDS.  Wavefront w fills row blocks 4w .. 4w+3 (8 rows of
+    // 128 B) of both operand tiles; lane l writes physical chunk l % 8 of row
+    // l / 8 of a block, which holds logical chunk (l % 8) ^ ((row / 2) % 8).
+    // Offsets are 32-bit bytes from the resource base; the k offset of a
+    // k-tile is the scalar offset.  The host routes larger operands to the
+    // narrow kernel.
+    const uint16_t* A = reinterpret_cast<const uint16_t*>(a.A);
+    const uint16_t* B = reinterpret_cast<const uint16_t*>(a.B);
+    int64_t a_bytes;
+    const uint16_t* abase;
+    if constexpr (GATHER) {
+        abase = A;
+        a_bytes = a.arow_count * a.lda * 2;
+    } else {
+        abase = A + (int64_t)m0 * a.lda;
+        a_bytes = (int64_t)(a.M - m0) * a.lda * 2;
+    }
+    const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)abase, (short)0, (int)(a_bytes < (int64_t)kBadRow ? a_bytes : (int64_t)kBadRow - 1), kBufWord3);
+    const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(B + (int64_t)n0 * a.ldb), (short)0, (int)(kWBN * a.ldb * 2), kBufWord3);
+    uint32_t ao[4], bo[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int row = (w * 4 + i) * 8 + (lane >> 3);
+        const int c = (lane & 7) ^ ((row >> 1) & 7);
+        if constexpr (GATHER) {
+            const int m = m0 + row;
+            int32_t r = m < a.M ? a.arows[m] : -1;
+            ao[i] = (r >= 0 && r < a.arow_count) ? (uint32_t)((int64_t)r * a.lda * 2 + c * 16) : kBadRow;
+        } else {
+            ao[i] = (uint32_t)(row * a.lda * 2 + c * 16);
+        }
+        bo[i] = (uint32_t)(row * a.ldb * 2 + c * 16);
+    }
+    const int dst = w * 4 * 1024;
+    auto issue = [&](lds_t* sa, lds_t* sb, int k0) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void*)(sa + dst + i * 1024), 16, ao[i], k0 * 2, 0, 0);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_void*)(sb + dst + i * 1024), 16, bo[i], k0 * 2, 0, 0);
+    };
+
+    // ---- fragment reads: lane l reads row l % 32 of a 32-row block, logical
+    // chunk 2 kk + l / 32, which sits at physical chunk (2 kk + l / 32) ^ sw.
+    const int l31 = lane & 31, half = lane >> 5;
+    const int sw = (l31 >> 1) & 7, shi = sw >> 1, slo = sw & 1;
+    int offA[4], offB[4];
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+        const int cb = 32 * (kk ^ shi) + 16 * (half ^ slo);
+        offA[kk] = (wm * 128 + l31) * 128 + cb;
+        offB[kk] = (wn * 64 + l31) * 128 + cb;
+    }
+
+    f32x16 acc[4][2];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+    // One k-tile: the fragments of step kk+1 are read before the MFMAs of step
+    // kk (the scheduling barriers keep that order).
+    auto compute = [&](const lds_t* sa, const lds_t* sb) {
+        bf16x8 fa[2][4], fb[2][2];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) fa[0][i] = *(const lds_frag*)(sa + offA[0] + i * 4096);
+#pragma unroll
+        for (int j = 0; j < 2; ++j) fb[0][j] = *(const lds_frag*)(sb + offB[0] + j * 4096);
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+            const int cur = kk & 1, nxt = cur ^ 1;
+            if (kk < 3) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) fa[nxt][i] = *(const lds_frag*)(sa + offA[kk + 1] + i * 4096);
+#pragma unroll
+                for (int j = 0; j < 2; ++j) fb[nxt][j] = *(const lds_frag*)(sb + offB[kk + 1] + j * 4096);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cur][i], fb[cur][j], acc[i][j], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    };
+
+    // Two stages.  Before each k-tile every wavefront waits for its own
+    // LDS-destination loads, then the barrier makes all of them visible and
+    // guarantees the other stage is no longer read: the next k-tile's loads go
+    // there while this one is computed.
+    // The host sends only an even number of k-tiles (K % 128 == 0) here: a
+    // loop with a single exit keeps the accumulators in place.
+    const int KT = a.K / kBK;
+    issue(a0, b0, 0);
+    for (int kt = 0; kt < KT; kt += 2) {
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+        issue(a1, b1, (kt + 1) * kBK);
+        compute(a0, b0);
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+        if (kt + 2 < KT) issue(a0, b0, (kt + 2) * kBK);
+        compute(a1, b1);
+    }
+
+    // ---- epilogue (the narrow kernel's, over four N-quarters) --------------
+    // The row strides pass through an empty asm so that no output address is
+    // formed before the main loop (64 row offsets held across it would spill).
+    int64_t ldc = a.ldc, ldp = a.ldp;
+    asm volatile("" : "+s"(ldc), "+s"(ldp));
+    uint16_t* C = reinterpret_cast<uint16_t*>(a.C);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            const int rl = wm * 128 + i * 32 + (v >> 2) * 8 + half * 4 + (v & 3);   // row in the tile
+            const int m = m0 + rl;
+            const bool ok = m < a.M;
+            float dot = 0.f, pp = 0.f, cc = 0.f;
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const int n = n0 + wn * 64 + j * 32 + l31;
+                const float c = acc[i][j][v];
+                if (ok) C[(int64_t)m * ldc + n] = to_bf16(c);
+                if constexpr (COS) {
+                    const float p = ok ? bf16_lo(reinterpret_cast<const uint16_t*>(a.P)[(int64_t)m * ldp + n]) : 0.f;
+                    dot = fmaf(p, c, dot);
+                    pp = fmaf(p, p, pp);
+                    cc = fmaf(c, c, cc);
+                }
+            }
+            if constexpr (COS) {
+                dot = half_sum(dot);
+                pp = half_sum(pp);
+                cc = half_sum(cc);
+                if (l31 == 31) {
+                    float* r = red + ((size_t)wn * kBM + rl) * 3;
+                    r[0] = dot;
+                    r[1] = pp;
+                    r[2] = cc;
+                }
+            }
+        }
+        // one 32-row block at a time: keeps the X_pre loads of later blocks
+        // from being hoisted (and their registers spilled)
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    if constexpr (COS) {
+        __syncthreads();
+        // one thread per tile row: the four N-quarters in order, then this
+        // tile's partials
+        if (tid < kBM) {
+            const int m = m0 + tid;
+            if (m < a.M) {
+                float d = 0.f, p = 0.f, q = 0.f;
+#pragma unroll
+                for (int qn = 0; qn < 4; ++qn) {
+                    const float* r = red + ((size_t)qn * kBM + tid) * 3;
+                    d += r[0];
+                    p += r[1];
+                    q += r[2];
+                }
+                float* out = a.part + ((int64_t)m * a.part_cols + n0 / kWBN) * 3;
+                out[0] = d;
+                out[1] = p;
+                out[2] = q;
+            }
+        }
+    }
+}
+
 // s = dot / (|P| |C|) from the per-tile partials, summed in tile order; the
 // same zero-norm reading as the scoring kernel (s = 0).
-__global__ __launch_bounds__(256) void cos_finish_kernel(const float* part, int cols, int M, float* s)
+__global__ __launch_bounds__(256) void cos_finish_kernel(const float* part, int stride, int cols, int M, float* s)
 {
     const int m = blockIdx.x * blockDim.x + threadIdx.x;
     if (m >= M) return;
-    const float* p = part + (int64_t)m * cols * 3;
+    const float* p = part + (int64_t)m * stride * 3;
     float dot = 0.f, n1 = 0.f, n2 = 0.f;
     for (int c = 0; c < cols; ++c) {
         dot += p[3 * c];
@@ -228,8 +448,20 @@ __global__ __launch_bounds__(256) void cos_finish_kernel(const float* part, int 
     s[m] = v;
 }
 
+// The wide kernel takes the shape when N is a multiple of 256, K of 128 (an
+// even number of k-tiles) and every buffer offset it forms fits 31 bits.
+bool use_wide(const GemmArgs& a)
+{
+    if (a.N % kWBN || a.K % (2 * kBK)) return false;
+    const int64_t lim = (int64_t)kBadRow;
+    if ((int64_t)kBM * a.lda * 2 >= lim || (int64_t)kWBN * a.ldb * 2 >= lim) return false;
+    if (a.arows && a.arow_count * a.lda * 2 >= lim) return false;
+    return true;
+}
+
 }  // namespace
 
+// capacity (row stride of the partials): the narrow kernel's column count
 int gemm_part_cols(int N) { return N / kBN; }
 
 bool gemm_shape_ok(int M, int N, int K)
@@ -255,21 +487,32 @@ hipError_t gemm_prepare()
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t s)
 {
     if (a.M == 0) return hipSuccess;
-    const int tiles = ((a.M + kBM - 1) / kBM) * (a.N / kBN);
-    const int grid = ((tiles + kXcds - 1) / kXcds) * kXcds;
     const bool gather = a.arows != nullptr, cos = a.P != nullptr;
-    const size_t lds = kLdsA + kLdsB + (cos ? kLdsRed : 0);
     if (gather && cos) return hipErrorInvalidValue;
-    if (gather)
-        hipLaunchKernelGGL((gemm_kernel<true, false>), dim3(grid), dim3(kThreads), lds, s, a);
-    else if (cos)
-        hipLaunchKernelGGL((gemm_kernel<false, true>), dim3(grid), dim3(kThreads), lds, s, a);
-    else
-        hipLaunchKernelGGL((gemm_kernel<false, false>), dim3(grid), dim3(kThreads), lds, s, a);
+    const bool wide = use_wide(a);
+    const int bn = wide ? kWBN : kBN;
+    const int tiles = ((a.M + kBM - 1) / kBM) * (a.N / bn);
+    const int grid = ((tiles + kXcds - 1) / kXcds) * kXcds;
+    if (wide) {
+        if (gather)
+            hipLaunchKernelGGL((gemm_wide_kernel<true, false>), dim3(grid), dim3(kWThreads), 0, s, a);
+        else if (cos)
+            hipLaunchKernelGGL((gemm_wide_kernel<false, true>), dim3(grid), dim3(kWThreads), 0, s, a);
+        else
+            hipLaunchKernelGGL((gemm_wide_kernel<false, false>), dim3(grid), dim3(kWThreads), 0, s, a);
+    } else {
+        const size_t lds = kLdsA + kLdsB + (cos ? kLdsRed : 0);
+        if (gather)
+            hipLaunchKernelGGL((gemm_kernel<true, false>), dim3(grid), dim3(kThreads), lds, s, a);
+        else if (cos)
+            hipLaunchKernelGGL((gemm_kernel<false, true>), dim3(grid), dim3(kThreads), lds, s, a);
+        else
+            hipLaunchKernelGGL((gemm_kernel<false, false>), dim3(grid), dim3(kThreads), lds, s, a);
+    }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || !cos) return e;
-    hipLaunchKernelGGL(cos_finish_kernel, dim3((a.M + 255) / 256), dim3(256), 0, s, a.part, a.part_cols, a.M,
-                       a.s_out);
+    hipLaunchKernelGGL(cos_finish_kernel, dim3((a.M + 255) / 256), dim3(256), 0, s, a.part, a.part_cols, a.N / bn,
+                       a.M, a.s_out);
     return hipGetLastError();
 }
 

@@ -72,7 +72,7 @@ struct GemmArgs {
     const void* P;           // bf16 [M, N] (stride ldp) for the cosine epilogue, or nullptr
     int64_t ldp;
     float* part;             // [M, part_cols, 3] cosine partials (with P)
-    int32_t part_cols;       // N / 128
+    int32_t part_cols;       // row stride of part: N / 128 (the wide kernel fills N / 256)
     float* s_out;            // [M] cosine of the rows of P and C (with P)
 };
 

@@ -55,8 +55,11 @@ def check_gemm(C, A_rows, B):
     assert not bad.any(), "%d outputs outside the bound, first at %s" % (bad.sum(), np.argwhere(bad)[:3])
 
 
+# N % 256 == 0 with K % 128 == 0 runs the wide tiling (256 x 256, LDS-destination
+# loads), every other shape the narrow one (256 x 128, register prefetch).
 @pytest.mark.parametrize("M,N,K,pad", [(1, 128, 64, 0), (300, 256, 128, 0), (257, 384, 512, 8),
-                                       (1000, 1024, 4096, 0), (4096, 4096, 4096, 0)])
+                                       (130, 256, 192, 0), (257, 512, 512, 8), (1000, 1024, 4096, 0),
+                                       (4096, 4096, 4096, 0)])
 def test_gemm_matches_fp64(M, N, K, pad):
     say("gemm", M, N, K, "pad", pad)
     g = torch.Generator().manual_seed(M + N + K)
@@ -70,11 +73,12 @@ def test_gemm_matches_fp64(M, N, K, pad):
     r.close()
 
 
-def test_gemm_gathered_rows():
-    say("gemm gather 777 x 384 x 512")
+@pytest.mark.parametrize("N", [384, 512])
+def test_gemm_gathered_rows(N):
+    say("gemm gather 777 x %d x 512" % N)
     g = torch.Generator().manual_seed(3)
     A = randn_bf16(g, 900, 512)
-    B = randn_bf16(g, 384, 512)
+    B = randn_bf16(g, N, 512)
     rows = torch.randint(-3, 905, (777,), generator=g, dtype=torch.int32)   # duplicates and out-of-range
     r = reducer()
     C = r.gemm(A.to(DEV), B.to(DEV), rows=rows.to(DEV))
@@ -84,6 +88,24 @@ def test_gemm_gathered_rows():
     Ag[ok] = A[rows[ok].long()]
     check_gemm(C, Ag, B)
     assert torch.count_nonzero(C[~ok.to(DEV)]) == 0
+    r.close()
+
+
+def test_gemm_tilings_agree_bit_for_bit():
+    """The wide (N % 256 == 0) and narrow (N % 256 == 128) tilings run the same
+    MFMA sequence for every output element, so the columns they share are
+    bit-identical, plain and gathered."""
+    say("gemm wide vs narrow 1000 x 512/384 x 1024")
+    g = torch.Generator().manual_seed(11)
+    A = randn_bf16(g, 1000, 1024).to(DEV)
+    B = randn_bf16(g, 512, 1024).to(DEV)
+    rows = torch.randint(-2, 1003, (600,), generator=g, dtype=torch.int32).to(DEV)
+    r = reducer()
+    wide, narrow = r.gemm(A, B), r.gemm(A, B[:384])
+    gw, gn = r.gemm(A, B, rows=rows), r.gemm(A, B[:384], rows=rows)
+    torch.cuda.synchronize()
+    assert torch.equal(wide[:, :384].view(torch.int16), narrow.view(torch.int16))
+    assert torch.equal(gw[:, :384].view(torch.int16), gn.view(torch.int16))
     r.close()
 
 
