@@ -91,11 +91,15 @@ def test_gemm_gathered_rows(N):
     r.close()
 
 
-def test_gemm_tilings_agree_bit_for_bit():
+@pytest.mark.parametrize("tile_rows", [None, 128, 192, 256])
+def test_gemm_tilings_agree_bit_for_bit(tile_rows, monkeypatch):
     """The wide (N % 256 == 0) and narrow (N % 256 == 128) tilings run the same
     MFMA sequence for every output element, so the columns they share are
-    bit-identical, plain and gathered."""
-    say("gemm wide vs narrow 1000 x 512/384 x 1024")
+    bit-identical, plain and gathered, at every tile height of the wide one
+    (TR_GEMM_TILE_ROWS pins it; None leaves it to the model)."""
+    if tile_rows is not None:
+        monkeypatch.setenv("TR_GEMM_TILE_ROWS", str(tile_rows))
+    say("gemm wide vs narrow 1000 x 512/384 x 1024, tile rows", tile_rows)
     g = torch.Generator().manual_seed(11)
     A = randn_bf16(g, 1000, 1024).to(DEV)
     B = randn_bf16(g, 512, 1024).to(DEV)
@@ -132,6 +136,18 @@ def mlp_inputs(M, Dc, Hd, seed):
 
 @pytest.mark.parametrize("M,Dc,Hd", [(1000, 1024, 4096), (333, 256, 512), (64, 128, 64)])
 def test_mlp_out_cos_parity(M, Dc, Hd):
+    run_mlp_out_cos_parity(M, Dc, Hd)
+
+
+@pytest.mark.parametrize("tile_rows", [128, 192, 256])
+def test_mlp_out_cos_parity_each_tile_height(tile_rows, monkeypatch):
+    """The cosine epilogue stages P through LDS by 128-row halves; 192-row
+    tiles split a wavefront's rows across both stages."""
+    monkeypatch.setenv("TR_GEMM_TILE_ROWS", str(tile_rows))
+    run_mlp_out_cos_parity(1000, 512, 256)
+
+
+def run_mlp_out_cos_parity(M, Dc, Hd):
     say("mlp_out_cos", M, Dc, Hd)
     Xpre, H, W2 = mlp_inputs(M, Dc, Hd, M + Dc)
     Xpre[5] = 0                                                   # zero-norm x': s = 0
