@@ -382,6 +382,28 @@ def main():
     stage_ms, calls = r.timing_read()
     r.timing(False)
 
+    # Serving form: one step captured in a HIP graph (tr_reduce allocates and
+    # copies nothing, so it captures), replayed K times: the same kernels on
+    # the same inputs, one graph launch per step from the host.
+    side = torch.cuda.Stream(dev)
+    side.wait_stream(stream)
+    with torch.cuda.stream(side):
+        step()
+    stream.wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=side):
+        step()
+    for _ in range(3):
+        graph.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        graph.replay()
+    torch.cuda.synchronize()
+    g_elapsed = time.perf_counter() - t0
+    del graph
+
     ms_step = 1e3 * elapsed / args.steps
     images_s = w.B * args.steps / elapsed
     rows = sum(w.N)
@@ -420,6 +442,8 @@ def main():
                      "frac": round(path_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
         "step_ms_events": {"median": round(pick(0.5), 5), "p10": round(pick(0.1), 5),
                            "p90": round(pick(0.9), 5), "steps": len(step_ev)},
+        "graph_replay": {"ms_per_step": round(1e3 * g_elapsed / args.steps, 5),
+                         "images_per_s": round(w.B * args.steps / g_elapsed, 1)},
         "stage_ms_with_events": {"score": round(stage_ms[0] / max(calls, 1), 5),
                                  "select": round(stage_ms[1] / max(calls, 1), 5),
                                  "gather": round(stage_ms[2] / max(calls, 1), 5)},
