@@ -1,7 +1,7 @@
 """Coefficients of the polynomial the scoring kernel uses for the Shannon term.
 
 phi(e) = g(1 + e) / e^2 with g(u) = u log u - u + 1, on |e| <= 1/4, as a
-degree-7 polynomial in e: the Chebyshev interpolant at 2000 Chebyshev nodes
+degree-5 polynomial in e: the Chebyshev interpolant at 2000 Chebyshev nodes
 (fp64), converted to monomial coefficients.  Prints the coefficients and the
 maximum relative error of phi over the interval (fp64 evaluation, then fp32
 Horner with fused multiply-adds).  Only numpy is needed.
@@ -10,7 +10,7 @@ import numpy as np
 from numpy.polynomial import chebyshev
 
 A = 0.25
-DEG = 7
+DEG = 5
 
 
 def phi(e):

@@ -133,23 +133,23 @@ __device__ __forceinline__ void x_chunk(XAcc& a, const float* v, int m, float c)
 }
 
 // g(1 + e) = (1 + e) log(1 + e) - e >= 0, given e (and u = 1 + e for the
-// direct form).  For |e| < 1/4 as e^2 phi(e), phi a degree-7 polynomial (the
+// direct form).  For |e| < 1/4 as e^2 phi(e), phi a degree-5 polynomial (the
 // Chebyshev interpolant of g(1 + e) / e^2 on [-1/4, 1/4], relative error
-// 3e-9; coefficients from gen_shannon_poly.py), which keeps full relative
-// accuracy where the direct form cancels; elsewhere u log u - e with the
+// 3e-7, 4e-7 with fp32 Horner; coefficients from gen_shannon_poly.py), which
+// keeps full relative accuracy where the direct form cancels (in fp32 the
+// direct form's error grows to 1e-5 at |e| = 1/8, so the cut stays at 1/4);
+// elsewhere u log u - e with the
 // hardware base-2 logarithm (argument clamped to 1e-30, a normal number, so
 // u = 0 gives 0 - e = 1).  Both forms are evaluated and one is selected: no
 // per-element divergence.
 __device__ __forceinline__ float g_shannon(float e, float u)
 {
-    float p = -1.525888537e-02f;
-    p = fmaf(p, e, 1.933413531e-02f);
-    p = fmaf(p, e, -2.374382957e-02f);
-    p = fmaf(p, e, 3.327445834e-02f);
-    p = fmaf(p, e, -5.000115357e-02f);
-    p = fmaf(p, e, 8.333407677e-02f);
-    p = fmaf(p, e, -1.666666612e-01f);
-    p = fmaf(p, e, 4.999999985e-01f);
+    float p = -2.541277015e-02f;
+    p = fmaf(p, e, 3.508703353e-02f);
+    p = fmaf(p, e, -4.994899918e-02f);
+    p = fmaf(p, e, 8.329159454e-02f);
+    p = fmaf(p, e, -1.666670687e-01f);
+    p = fmaf(p, e, 5.000001460e-01f);
     const float series = (e * e) * p;
     constexpr float kLn2 = 0.693147180559945309f;
     const float direct = fmaf(u * kLn2, __builtin_amdgcn_logf(fmaxf(u, 1e-30f)), -e);
