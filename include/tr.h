@@ -184,7 +184,11 @@ tr_status tr_select(tr_ctx* ctx, const float* key_imp, const float* key_s,
  *   C      device bf16 [M, N] (row stride ldc)
  * N must be a multiple of 128 and K of 64, and ceil(M / 256) * N / 128 must
  * stay below 2^31 (else TR_EUNSUPPORTED); A and B bases and row strides must
- * be 16-byte aligned (else TR_EINVAL). */
+ * be 16-byte aligned (else TR_EINVAL).  Every tiling the library picks for a
+ * shape gives the same bits (one fp32 accumulation order per element).  The
+ * environment variable TR_GEMM_TILE_ROWS = 128, 192 or 256, read by
+ * tr_create, pins the tile height of the tiling used when N % 256 == 0 and
+ * K % 128 == 0 (otherwise the height that fills the CUs best is taken). */
 tr_status tr_gemm_bf16(tr_ctx* ctx, const void* A, int64_t lda,
                        const int32_t* a_rows, int64_t a_row_count,
                        const void* B, int64_t ldb, void* C, int64_t ldc,
