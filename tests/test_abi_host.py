@@ -181,3 +181,27 @@ def test_read_bandwidth_validates_before_touching_a_device():
     assert lib.tr_read_bandwidth(ctypes.c_void_p(256), 16, sink, 0, None) == _lib.TR_EINVAL
     assert lib.tr_read_bandwidth(ctypes.c_void_p(256), 16, ctypes.c_void_p(66), 1, None) == _lib.TR_EINVAL
     assert b"16" in lib.tr_last_error()
+
+
+def test_last_error_is_per_thread():
+    """tr_last_error reports the calling thread's latest failure only."""
+    import threading
+    lib = _lib.load()
+    seen = {}
+
+    def failing():
+        assert lib.tr_read_bandwidth(None, -16, None, 0, None) == _lib.TR_EINVAL
+        seen["failing"] = lib.tr_last_error()
+
+    def quiet():
+        seen["quiet_before"] = lib.tr_last_error()
+        t = threading.Thread(target=failing)
+        t.start()
+        t.join()
+        seen["quiet_after"] = lib.tr_last_error()
+
+    t = threading.Thread(target=quiet)
+    t.start()
+    t.join()
+    assert seen["failing"] != b""
+    assert seen["quiet_before"] == b"" and seen["quiet_after"] == b""

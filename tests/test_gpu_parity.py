@@ -410,6 +410,48 @@ def test_reduce_replays_from_a_hip_graph(name, kw):
     r.close()
 
 
+def test_two_contexts_run_concurrently_from_two_threads():
+    """Distinct contexts are independent: two of them, each driven from its own
+    host thread on its own stream (the library call releases Python's lock),
+    reproduce their single-threaded results bit for bit."""
+    import threading
+    say("two contexts, two threads")
+    cases = [synth.make("llava", device=DEV, B=8, N=576, D=4096, K=64),
+             synth.make("qwen_ragged", device=DEV, B=5, n_lo=256, n_hi=6000, D=1024)]
+    reducers = [reducer_for(w) for w in cases]
+    ref = [r.reduce(w.X, w.Xpre, w.Xpost, w.N, w.K) for r, w in zip(reducers, cases)]
+    torch.cuda.synchronize()
+    got = [[], []]
+    errors = []
+
+    def worker(k):
+        try:
+            s = torch.cuda.Stream()
+            w, r = cases[k], reducers[k]
+            with torch.cuda.stream(s):
+                for _ in range(20):
+                    res = r.reduce(w.X, w.Xpre, w.Xpost, w.N, w.K)
+                    got[k].append((res.out.clone(), res.idx.clone(), res.src.clone()))
+            s.synchronize()
+        except Exception as e:   # reported by the main thread
+            errors.append(e)
+
+    threads = [threading.Thread(target=worker, args=(k,)) for k in range(2)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    torch.cuda.synchronize()
+    assert not errors, errors
+    for k in range(2):
+        assert len(got[k]) == 20
+        for out, idx, src in got[k]:
+            assert torch.equal(_bytes(out), _bytes(ref[k].out))
+            assert torch.equal(idx, ref[k].idx) and torch.equal(src, ref[k].src)
+    for r in reducers:
+        r.close()
+
+
 # ------------------------------------------- lambda extremes and stride variant
 
 LAM_CASES = [
