@@ -1,0 +1,65 @@
+"""Seeded random parity sweep: many small batches of mixed shape through
+tr_reduce, each checked against the fp64 oracle with the parity protocol
+(tests/parity.py).  The cases mix image sizes from 1 to 18432 tokens, row
+widths that are and are not multiples of the vector width, bf16 and fp32,
+lambda in [0, 1], K from 1 to N, both stride readings and both entropies,
+with exact duplicate rows and all-zero rows sprinkled in."""
+import random
+import sys
+
+import pytest
+import torch
+
+import parity
+import synth
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+def case(c, seed):
+    rng = random.Random(seed * 1_000_003 + c)
+    B = rng.choice([1, 2, 3, 5, 8])
+    D = rng.choice([8, 37, 64, 200, 520, 1024, 1032, 3584])
+    Dc = rng.choice([D, D, 16, 96, 333])
+    dtype = rng.choice([torch.bfloat16, torch.float32])
+    budget = 4_000_000 // max(D, Dc)
+    Ns = [max(1, min(rng.choice([1, 2, 7, 64, 65, 300, 576, 1000, 2880, 4100, 9000, 18432]), budget // B))
+          for _ in range(B)]
+    lam = rng.choice([0.0, 1.0, 1 / 3, 0.5, 0.9, rng.random()])
+    Ks = [max(1, min(n, rng.choice([1, 2, n // 9 + 1, n // 3 + 1, n]))) for n in Ns]
+    stride_mode = rng.choice([0, 0, 1])
+    entropy = rng.choice([2, 2, 1])
+    g = torch.Generator(device="cpu").manual_seed(1000 + c + 7919 * seed)
+    rows = sum(Ns)
+    X = torch.randn(rows, D, generator=g) * torch.exp(torch.randn(rows, 1, generator=g))
+    P = torch.randn(rows, Dc, generator=g)
+    Q = P + rng.choice([0.1, 1.0, 3.0]) * torch.randn(rows, Dc, generator=g)
+    for _ in range(rng.choice([0, 3, 20])):           # exact duplicates
+        i, j = rng.randrange(rows), rng.randrange(rows)
+        X[i], P[i], Q[i] = X[j], P[j], Q[j]
+    for _ in range(rng.choice([0, 2])):               # all-zero rows
+        X[rng.randrange(rows)] = 0
+    cast = lambda t: t.to(dtype).to(DEV).contiguous()
+    w = synth.Workload("sweep", cast(X), cast(P), cast(Q), Ns, Ks, lam)
+    return w, dtype, stride_mode, entropy
+
+
+@pytest.mark.parametrize("c", range(60))
+def test_random_case_matches_oracle(c):
+    import paper_2607_13500_amd as tr
+    w, dtype, stride_mode, entropy = case(c, seed=1)
+    print("[case] sweep %d: B=%d N=%s D=%d Dc=%d %s lam=%.3f K=%s stride=%d entropy=%d"
+          % (c, len(w.N), w.N, w.D, w.Dc, str(dtype).split(".")[-1], w.lam, w.K, stride_mode, entropy),
+          flush=True)
+    sys.stdout.flush()
+    r = tr.Reducer(w.D, w.Dc, dtype, lam=w.lam, max_images=len(w.N), max_tokens=sum(w.N),
+                   max_N=max(w.N), stride_real=bool(stride_mode), shannon=(entropy == 1))
+    res = r.reduce(w.X, w.Xpre, w.Xpost, w.N, w.K, want_scores=True)
+    key1, _, _ = r.score(w.X, w.Xpre, w.Xpost, want_h2=True)
+    torch.cuda.synchronize()
+    ref = parity.oracle_reference(w, stride_mode=stride_mode, entropy=entropy)
+    rep = parity.check(w, res, ref, cv2_gpu=key1, stride_mode=stride_mode, entropy=entropy)
+    print("   ", rep.summary(), flush=True)
+    assert rep.ok(), rep.failures[:5]
+    r.close()
