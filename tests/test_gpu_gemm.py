@@ -262,3 +262,41 @@ def test_mlp_out_cos_rejects_bad_requests():
         r.mlp_out_cos(H, torch.zeros(128, 64, dtype=torch.bfloat16, device=DEV),
                       torch.zeros(100, 128, dtype=torch.float32, device=DEV))
     r.close()
+
+
+@pytest.mark.parametrize("c", range(24))
+def test_gemm_random_shapes(c, monkeypatch):
+    """Seeded random shapes: M from 1 to 5000, N and K over their allowed
+    multiples, padded row strides, gathered rows with duplicates and
+    out-of-range indices, each tile height; against the float64 product."""
+    import random
+    rng = random.Random(7000 + c)
+    tile = rng.choice([None, 128, 192, 256])
+    if tile is not None:
+        monkeypatch.setenv("TR_GEMM_TILE_ROWS", str(tile))
+    M = rng.choice([1, 31, 64, 200, 257, 1000, 2049, 5000])
+    N = 128 * rng.choice([1, 2, 3, 4, 8, 12])
+    K = 64 * rng.choice([1, 2, 3, 4, 8, 16])
+    pad = rng.choice([0, 0, 8, 24])
+    gather = rng.random() < 0.4
+    say("gemm random", c, M, N, K, "pad", pad, "gather", gather, "tile rows", tile)
+    g = torch.Generator().manual_seed(7000 + c)
+    R = M + rng.choice([0, 7, 300]) if gather else M
+    A = randn_bf16(g, R, K + pad)
+    B = randn_bf16(g, N, K + pad)
+    r = reducer()
+    Ad, Bd = A.to(DEV), B.to(DEV)
+    if gather:
+        rows = torch.randint(-2, R + 3, (M,), generator=g, dtype=torch.int32)
+        C = r.gemm(Ad[:, :K], Bd[:, :K], rows=rows.to(DEV))
+        ok = (rows >= 0) & (rows < R)
+        Ag = torch.zeros(M, K, dtype=torch.bfloat16)
+        Ag[ok] = A[rows[ok].long(), :K]
+        torch.cuda.synchronize()
+        check_gemm(C, Ag, B[:, :K].contiguous())
+        assert torch.count_nonzero(C[~ok.to(DEV)]) == 0
+    else:
+        C = r.gemm(Ad[:, :K], Bd[:, :K])
+        torch.cuda.synchronize()
+        check_gemm(C, A[:, :K].contiguous(), B[:, :K].contiguous())
+    r.close()
