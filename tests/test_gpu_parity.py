@@ -56,6 +56,7 @@ SMALL = [
     ("llava_next", dict(B=2, D=4096, K=320)),
     ("qwen_ragged", dict(B=5, n_lo=256, n_hi=3000, D=3584)),
     ("video", dict(B=1, frames=6, positions=576, D=4096, K=216)),
+    ("llava", dict(B=2, N=300, D=4096, K=40, dtype=torch.float32)),   # 16 KiB rows: one per wavefront
 ]
 
 
