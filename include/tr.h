@@ -252,13 +252,15 @@ int32_t tr_capacity_N(void);
 tr_status tr_timing_enable(tr_ctx* ctx, int32_t enable);
 tr_status tr_timing_read(tr_ctx* ctx, double* ms, int64_t* calls);
 
-/* Measurement hook: read `bytes` (a multiple of 16) at device address p
- * (16-byte aligned) once, with 16-byte non-temporal loads and nothing else,
- * on `stream`: the streaming-read ceiling the scoring kernel's bandwidth is
- * compared with.  sink is device scratch of sink_words uint32 (>= 1) that the
- * kernel may write; its contents are meaningless.  Needs no context. */
-tr_status tr_read_bandwidth(const void* p, int64_t bytes, uint32_t* sink,
-                            int32_t sink_words, void* stream);
+/* Measurement hook: read n buffers (1 <= n <= 8; host arrays p of device
+ * addresses, 16-byte aligned, and bytes, each a multiple of 16) once, in one
+ * kernel launch on `stream`, with 16-byte non-temporal loads and nothing
+ * else: the streaming-read ceiling the scoring kernel's bandwidth is compared
+ * with (the scoring kernel also reads its three tensors in one launch).  sink
+ * is device scratch of sink_words uint32 (>= 1) that the kernel may write;
+ * its contents are meaningless.  Needs no context. */
+tr_status tr_read_bandwidth(const void* const* p, const int64_t* bytes, int32_t n,
+                            uint32_t* sink, int32_t sink_words, void* stream);
 
 /* Release the context and its scratch (NULL is a no-op).  Freeing device
  * memory waits for the device to finish outstanding work first. */

@@ -72,15 +72,18 @@ def plan(N: Sequence[int], K: Optional[Sequence[int]] = None, lam: float = LAMBD
 
 
 def read_bandwidth(buffers, stream=None) -> None:
-    """Measurement hook: read each (16-byte aligned, contiguous) device tensor
-    once with the streaming-read kernel (the read ceiling of the device)."""
+    """Measurement hook: read the (16-byte aligned, contiguous) device tensors
+    once, in one kernel launch (the streaming-read ceiling of the device)."""
     lib = _lib.load()
+    if not 1 <= len(buffers) <= 8:
+        raise ValueError("read_bandwidth takes 1 to 8 tensors")
     sink = torch.empty(4096, dtype=torch.int32, device=buffers[0].device)
     st = stream if stream is not None else torch.cuda.current_stream(buffers[0].device)
-    for b in buffers:
-        nbytes = b.numel() * b.element_size()
-        _check(lib.tr_read_bandwidth(_ptr(b), nbytes - nbytes % 16, _ptr(sink), sink.numel(),
-                                     ctypes.c_void_p(st.cuda_stream)), "tr_read_bandwidth")
+    n = len(buffers)
+    ptrs = (ctypes.c_void_p * n)(*[b.data_ptr() for b in buffers])
+    sizes = (ctypes.c_int64 * n)(*[(b.numel() * b.element_size()) // 16 * 16 for b in buffers])
+    _check(lib.tr_read_bandwidth(ctypes.cast(ptrs, ctypes.c_void_p), ctypes.cast(sizes, ctypes.c_void_p), n,
+                                 _ptr(sink), sink.numel(), ctypes.c_void_p(st.cuda_stream)), "tr_read_bandwidth")
 
 
 def capacity_N() -> int:

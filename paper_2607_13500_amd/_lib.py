@@ -67,7 +67,7 @@ def load(build_if_missing: bool = True) -> ctypes.CDLL:
     lib.tr_reduce_given_s.restype = i32
     lib.tr_reduce_project.argtypes = [vp, vp, vp, vp, i32, vp, vp, vp, i64, i32, vp, vp, vp, vp]
     lib.tr_reduce_project.restype = i32
-    lib.tr_read_bandwidth.argtypes = [vp, i64, vp, i32, vp]
+    lib.tr_read_bandwidth.argtypes = [vp, vp, i32, vp, i32, vp]
     lib.tr_read_bandwidth.restype = i32
     lib.tr_plan.argtypes = [P(Params), i32, vp, vp, vp, vp, vp, vp]
     lib.tr_plan.restype = i32

@@ -662,14 +662,22 @@ tr_status tr_mlp_out_cos(tr_ctx* c, const void* Hact, int64_t ldh, const void* W
     return TR_OK;
 }
 
-tr_status tr_read_bandwidth(const void* p, int64_t bytes, uint32_t* sink, int32_t sink_words, void* stream)
+tr_status tr_read_bandwidth(const void* const* p, const int64_t* bytes, int32_t n, uint32_t* sink,
+                            int32_t sink_words, void* stream)
 {
     g_err.clear();
-    if (bytes < 0 || bytes % 16) return fail(TR_EINVAL, "bytes must be a non-negative multiple of 16");
-    if (bytes == 0) return TR_OK;
-    if (!p || !aligned16(p) || !sink || sink_words < 1 || ((uintptr_t)sink & 3u))
-        return fail(TR_EINVAL, "p must be 16-byte aligned, sink a 4-byte aligned buffer of >= 1 word");
-    hipError_t e = tr::launch_read(p, bytes, sink, sink_words, static_cast<hipStream_t>(stream));
+    if (n < 1 || n > tr::kReadBuffers || !p || !bytes)
+        return fail(TR_EINVAL, "n must be in [1, %d] with host arrays p and bytes", tr::kReadBuffers);
+    int64_t total = 0;
+    for (int i = 0; i < n; ++i) {
+        if (bytes[i] < 0 || bytes[i] % 16) return fail(TR_EINVAL, "bytes[%d] must be a non-negative multiple of 16", i);
+        if (bytes[i] && (!p[i] || !aligned16(p[i]))) return fail(TR_EINVAL, "p[%d] must be 16-byte aligned", i);
+        total += bytes[i];
+    }
+    if (total == 0) return TR_OK;
+    if (!sink || sink_words < 1 || ((uintptr_t)sink & 3u))
+        return fail(TR_EINVAL, "sink must be a 4-byte aligned buffer of >= 1 word");
+    hipError_t e = tr::launch_read(p, bytes, n, sink, sink_words, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "read kernel launch");
     return TR_OK;
 }

@@ -58,7 +58,17 @@ hipError_t launch_gather(const void* X, void* out, const int32_t* rows, int64_t 
 // ---- measurement: streaming-read ceiling --------------------------------------
 // Reads bytes / 16 chunks of p (16-byte aligned) once; at most sink_words
 // workgroups, each of which may write sink[its index].
-hipError_t launch_read(const void* p, int64_t bytes, uint32_t* sink, int sink_words, hipStream_t s);
+// Buffers of one read-ceiling launch (at most kReadBuffers, each a whole
+// number of 16-byte chunks; span_end: running count of 8 KB spans).
+constexpr int kReadBuffers = 8;
+struct ReadSet {
+    const void* p[kReadBuffers];
+    int64_t chunks[kReadBuffers];
+    int64_t span_end[kReadBuffers];
+    int n;
+};
+hipError_t launch_read(const void* const* p, const int64_t* bytes, int n, uint32_t* sink, int sink_words,
+                       hipStream_t s);
 
 // ---- bf16 matrix-core GEMM: C[M, N] = A[M, K] . B[N, K]^T -----------------
 struct GemmArgs {

@@ -1,8 +1,8 @@
-// Measurement hook: the streaming-read ceiling of the device.  A kernel that
-// reads a buffer once with the scoring kernel's access style (single-wave
-// workgroups, 16-byte non-temporal loads, eight in flight per lane) and does
-// nothing else, so the scoring kernel's bandwidth can be set against what a
-// pure read of the same bytes achieves on this device.
+// Measurement hook: the streaming-read ceiling of the device.  One launch
+// that reads a set of buffers once with the scoring kernel's access style
+// (single-wave workgroups, 16-byte non-temporal loads, eight in flight per
+// lane) and does nothing else, so the scoring kernel's bandwidth can be set
+// against what a pure read of the same bytes achieves on this device.
 #include "tr_internal.h"
 
 namespace tr {
@@ -14,16 +14,21 @@ constexpr int kReadUnroll = 8;
 constexpr int64_t kSpanChunks = (int64_t)kWave * kReadUnroll;   // 8 KB per wavefront
 
 // One single-wave workgroup per 8 KB span (the grain of the scoring kernel's
-// rows): lane l reads chunks l, l + 64, ... of the span, all in flight at once.
-__global__ __launch_bounds__(64) void read_kernel(const u32x4* __restrict__ p, int64_t chunks,
-                                                  uint32_t* __restrict__ sink, int sink_words)
+// rows) of the concatenated buffers: lane l reads chunks l, l + 64, ... of
+// the span, all in flight at once.
+__global__ __launch_bounds__(64) void read_kernel(ReadSet r, uint32_t* __restrict__ sink, int sink_words)
 {
-    const int64_t c0 = (int64_t)blockIdx.x * kSpanChunks + threadIdx.x;
+    const int64_t span = blockIdx.x;
+    int i = 0;
+    while (i + 1 < r.n && span >= r.span_end[i]) ++i;   // wave-uniform
+    const int64_t first = i ? r.span_end[i - 1] : 0;
+    const u32x4* p = static_cast<const u32x4*>(r.p[i]);
+    const int64_t c0 = (span - first) * kSpanChunks + threadIdx.x;
     u32x4 v[kReadUnroll];
 #pragma unroll
     for (int u = 0; u < kReadUnroll; ++u) {
         const int64_t c = c0 + (int64_t)kWave * u;
-        v[u] = c < chunks ? __builtin_nontemporal_load(p + c) : u32x4{0u, 0u, 0u, 0u};
+        v[u] = c < r.chunks[i] ? __builtin_nontemporal_load(p + c) : u32x4{0u, 0u, 0u, 0u};
     }
     uint32_t acc = 0;
 #pragma unroll
@@ -34,14 +39,25 @@ __global__ __launch_bounds__(64) void read_kernel(const u32x4* __restrict__ p, i
 
 }  // namespace
 
-hipError_t launch_read(const void* p, int64_t bytes, uint32_t* sink, int sink_words, hipStream_t s)
+hipError_t launch_read(const void* const* p, const int64_t* bytes, int n, uint32_t* sink, int sink_words,
+                       hipStream_t s)
 {
-    const int64_t chunks = bytes / 16;
-    if (chunks <= 0) return hipSuccess;
-    const int64_t blocks = (chunks + kSpanChunks - 1) / kSpanChunks;
-    if (blocks > (int64_t)INT32_MAX) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(read_kernel, dim3((unsigned)blocks), dim3(kWave), 0, s, static_cast<const u32x4*>(p),
-                       chunks, sink, sink_words);
+    ReadSet r{};
+    int64_t spans = 0;
+    int m = 0;
+    for (int i = 0; i < n; ++i) {
+        const int64_t chunks = bytes[i] / 16;
+        if (chunks <= 0) continue;
+        r.p[m] = p[i];
+        r.chunks[m] = chunks;
+        spans += (chunks + kSpanChunks - 1) / kSpanChunks;
+        r.span_end[m] = spans;
+        ++m;
+    }
+    r.n = m;
+    if (m == 0) return hipSuccess;
+    if (spans > (int64_t)INT32_MAX) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(read_kernel, dim3((unsigned)spans), dim3(kWave), 0, s, r, sink, sink_words);
     return hipGetLastError();
 }
 

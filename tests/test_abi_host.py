@@ -168,19 +168,31 @@ def test_gemm_and_fused_entry_points_validate_before_touching_a_device():
     assert lib.tr_last_error() != b""
 
 
+def _read_args(ptrs, sizes):
+    n = len(ptrs)
+    p = (ctypes.c_void_p * max(n, 1))(*ptrs)
+    b = (ctypes.c_int64 * max(n, 1))(*sizes)
+    return ctypes.cast(p, ctypes.c_void_p), ctypes.cast(b, ctypes.c_void_p), n
+
+
 def test_read_bandwidth_validates_before_touching_a_device():
-    """The read hook rejects sizes and pointers it cannot stream, and reads
-    nothing for 0 bytes, all without a device call."""
+    """The read hook rejects sets, sizes and pointers it cannot stream, and
+    reads nothing for 0 bytes, all without a device call."""
     lib = _lib.load()
     sink = ctypes.c_void_p(64)   # never dereferenced: every call below returns first
-    assert lib.tr_read_bandwidth(None, 0, None, 0, None) == _lib.TR_OK
-    assert lib.tr_read_bandwidth(None, -16, sink, 1, None) == _lib.TR_EINVAL
-    assert lib.tr_read_bandwidth(ctypes.c_void_p(256), 24, sink, 1, None) == _lib.TR_EINVAL
-    assert lib.tr_read_bandwidth(None, 16, sink, 1, None) == _lib.TR_EINVAL
-    assert lib.tr_read_bandwidth(ctypes.c_void_p(264), 16, sink, 1, None) == _lib.TR_EINVAL
-    assert lib.tr_read_bandwidth(ctypes.c_void_p(256), 16, sink, 0, None) == _lib.TR_EINVAL
-    assert lib.tr_read_bandwidth(ctypes.c_void_p(256), 16, ctypes.c_void_p(66), 1, None) == _lib.TR_EINVAL
-    assert b"16" in lib.tr_last_error()
+    ok = lambda ptrs, sizes, sk=sink, words=1: lib.tr_read_bandwidth(*_read_args(ptrs, sizes), sk, words, None)
+    assert ok([None], [0], None, 0) == _lib.TR_OK                       # nothing to read
+    assert ok([None, None], [0, 0], None, 0) == _lib.TR_OK
+    assert lib.tr_read_bandwidth(None, None, 1, sink, 1, None) == _lib.TR_EINVAL   # no arrays
+    assert ok([], []) == _lib.TR_EINVAL                                  # n = 0
+    assert ok([256] * 9, [16] * 9) == _lib.TR_EINVAL                     # more than 8 buffers
+    assert ok([256], [-16]) == _lib.TR_EINVAL
+    assert ok([256], [24]) == _lib.TR_EINVAL                             # not a multiple of 16
+    assert ok([None], [16]) == _lib.TR_EINVAL
+    assert ok([256, 264], [16, 16]) == _lib.TR_EINVAL                    # misaligned second buffer
+    assert ok([256], [16], sink, 0) == _lib.TR_EINVAL                    # no sink words
+    assert ok([256], [16], ctypes.c_void_p(66), 1) == _lib.TR_EINVAL     # misaligned sink
+    assert b"sink" in lib.tr_last_error()
 
 
 def test_last_error_is_per_thread():
@@ -190,7 +202,7 @@ def test_last_error_is_per_thread():
     seen = {}
 
     def failing():
-        assert lib.tr_read_bandwidth(None, -16, None, 0, None) == _lib.TR_EINVAL
+        assert lib.tr_read_bandwidth(None, None, 0, None, 0, None) == _lib.TR_EINVAL
         seen["failing"] = lib.tr_last_error()
 
     def quiet():

@@ -658,15 +658,27 @@ def test_variants_parity_full_llava(name, opt):
 
 
 def test_read_bandwidth_hook():
+    import ctypes
     import paper_2607_13500_amd as tr
     from paper_2607_13500_amd import _lib
     say("read bandwidth hook")
     buf = torch.ones(1 << 20, dtype=torch.float32, device=DEV)
-    tr.read_bandwidth([buf, buf[: (1 << 19)]])
+    other = torch.ones(3000, dtype=torch.bfloat16, device=DEV)   # 6000 B: a partial last span
+    tr.read_bandwidth([buf, buf[: (1 << 19)], other])
     torch.cuda.synchronize()
     lib = _lib.load()
     sink = torch.empty(16, dtype=torch.int32, device=DEV)
-    assert lib.tr_read_bandwidth(buf.data_ptr(), 100, sink.data_ptr(), 16, None) == _lib.TR_EINVAL   # not a multiple of 16
-    assert lib.tr_read_bandwidth(buf.data_ptr() + 4, 64, sink.data_ptr(), 16, None) == _lib.TR_EINVAL   # misaligned
-    assert lib.tr_read_bandwidth(buf.data_ptr(), 64, sink.data_ptr(), 0, None) == _lib.TR_EINVAL   # no sink
-    assert lib.tr_read_bandwidth(buf.data_ptr(), 0, None, 0, None) == _lib.TR_OK                  # nothing to read
+
+    def call(ptrs, sizes, words=16):
+        n = len(ptrs)
+        p = (ctypes.c_void_p * n)(*ptrs)
+        b = (ctypes.c_int64 * n)(*sizes)
+        return lib.tr_read_bandwidth(ctypes.cast(p, ctypes.c_void_p), ctypes.cast(b, ctypes.c_void_p), n,
+                                     sink.data_ptr(), words, None)
+
+    assert call([buf.data_ptr()], [100]) == _lib.TR_EINVAL              # not a multiple of 16
+    assert call([buf.data_ptr() + 4], [64]) == _lib.TR_EINVAL           # misaligned
+    assert call([buf.data_ptr()], [64], words=0) == _lib.TR_EINVAL      # no sink
+    assert call([buf.data_ptr()], [0]) == _lib.TR_OK                    # nothing to read
+    assert call([buf.data_ptr(), other.data_ptr()], [64, 5984]) == _lib.TR_OK
+    torch.cuda.synchronize()
