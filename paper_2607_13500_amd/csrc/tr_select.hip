@@ -42,6 +42,9 @@ constexpr int kBuckets = kThreads;       // Stage II: value buckets (one per thr
 constexpr uint32_t kBucketLimit = 256;   // Stage II: largest bucket ranked by counting
 constexpr int kDenseRem = 4096;          // Stage II: rank whole buckets per wavefront from here
 constexpr int kSplitGroups = 16;         // workgroups sharing the ranking of one large image
+static_assert(kCountLimit <= (uint32_t)kThreads, "one thread per listed Stage I member");
+static_assert((kSplitGroups & (kSplitGroups - 1)) == 0, "split ownership is a mask");
+static_assert(kDenseRem / 2 >= 2 * kWave * kW, "dense ranking's pairs fit above the X^rem list");
 
 // ---- LDS layout (same arithmetic on host and device) -----------------------
 struct LdsLayout {
@@ -124,11 +127,48 @@ __device__ __forceinline__ bool is_leader(uint64_t m, int lane)
 
 __device__ __forceinline__ bool bit_of(const uint32_t* bm, int i) { return (bm[i >> 5] >> (i & 31)) & 1u; }
 
-// A wavefront writes the 64-bit ballot of tile `base` into two bitmap words.
+// A wavefront writes the 64-bit ballot of tile `base` into the tile's two
+// bitmap words (base is a multiple of 64 and every bitmap starts 8-byte
+// aligned, so the pair is one aligned 64-bit store).
 __device__ __forceinline__ void put_tile_bits(uint32_t* bm, int base, uint64_t bits, int lane)
 {
-    if (lane == 0) bm[base >> 5] = (uint32_t)bits;
-    if (lane == 32) bm[(base >> 5) + 1] = (uint32_t)(bits >> 32);
+    if (lane == 0) *reinterpret_cast<uint64_t*>(bm + (base >> 5)) = bits;
+}
+
+// bsel's words of tile `base` = bimp's words | bits.
+__device__ __forceinline__ void put_tile_union(uint32_t* bsel, const uint32_t* bimp, int base,
+                                               uint64_t bits, int lane)
+{
+    if (lane == 0)
+        *reinterpret_cast<uint64_t*>(bsel + (base >> 5)) =
+            *reinterpret_cast<const uint64_t*>(bimp + (base >> 5)) | bits;
+}
+
+// A wavefront's passes over its token range read kTileUnr tiles of 64 from
+// LDS before working on any of them, so the reads overlap.
+constexpr int kTileUnr = 4;
+
+// Keys base + 64 u + lane of v (u < kTileUnr); from `end` on, the key of
+// 0.0f, so that bucket arithmetic on them stays finite (callers mask them).
+__device__ __forceinline__ void load_tiles(const uint32_t* v, int base, int end, int lane,
+                                           uint32_t (&out)[kTileUnr])
+{
+#pragma unroll
+    for (int u = 0; u < kTileUnr; ++u) {
+        const int i = base + u * kWave + lane;
+        out[u] = i < end ? v[i] : 0x80000000u;
+    }
+}
+
+// Whether each of the same tokens is in X^rem (before `end`, not in bimp).
+__device__ __forceinline__ void rem_tiles(const uint32_t* bimp, int base, int end, int lane,
+                                          bool (&out)[kTileUnr])
+{
+#pragma unroll
+    for (int u = 0; u < kTileUnr; ++u) {
+        const int i = base + u * kWave + lane;
+        out[u] = i < end && !bit_of(bimp, i);
+    }
 }
 
 // Contiguous 64-aligned token range of wavefront w.
@@ -139,6 +179,26 @@ __device__ __forceinline__ void wave_range(int n, int w, int& beg, int& end)
     end = beg + seg < n ? beg + seg : n;
 }
 
+// Cross-wavefront reductions of one LDS row of per-wavefront values: lane l
+// reads entry l, the wavefront reduces in registers.
+static_assert(kW <= kWave, "one row entry per lane");
+
+// Sum of the entries of wavefronts 0 .. w-1.
+__device__ __forceinline__ uint32_t sum_before(const uint32_t* row, int w, int lane)
+{
+    return wave_sum_u32(lane < w ? row[lane] : 0u);
+}
+
+__device__ __forceinline__ uint32_t max_all(const uint32_t* row, int lane)
+{
+    return wave_max_u32(lane < kW ? row[lane] : 0u);
+}
+
+__device__ __forceinline__ uint32_t or_all(const uint32_t* row, int lane)
+{
+    return wave_or_u32(lane < kW ? row[lane] : 0u);
+}
+
 // Exclusive prefix over wavefronts of a per-wavefront count (each row of
 // slots is used once per kernel).
 __device__ __forceinline__ uint32_t wave_prefix(uint32_t count, uint32_t* row)
@@ -147,9 +207,7 @@ __device__ __forceinline__ uint32_t wave_prefix(uint32_t count, uint32_t* row)
     const int w = threadIdx.x / kWave;
     if (lane == 0) row[w] = count;
     __syncthreads();
-    uint32_t base = 0;
-    for (int i = 0; i < w; ++i) base += row[i];
-    return base;
+    return sum_before(row, w, lane);
 }
 
 struct Img {
@@ -173,20 +231,25 @@ __device__ __forceinline__ Img image_of(const SelectArgs& a, int local)
 // ---- phases ------------------------------------------------------------------
 // Load the image's keys (all global loads of a batch issued before the LDS
 // stores), zero `nzero` words at `zero`, and return the bits in which some key
-// differs from token 0's key.
-__device__ void load_keys(const SelectArgs& a, const Img& d, uint32_t* ki, uint32_t* ks,
-                          uint32_t* zero, int nzero, uint32_t* slots, uint32_t& k0i,
-                          uint32_t& VI, uint32_t& VS, uint32_t& kimin, uint32_t& kimax)
+// differs from token 0's key (each kind) and the range of the Stage I keys.
+struct KeyStats {
+    uint32_t k0i, VI, VS, kimin, kimax;
+};
+
+__device__ KeyStats load_keys(const SelectArgs& a, const Img& d, uint32_t* ki, uint32_t* ks,
+                              uint32_t* zero, int nzero, uint32_t* slots)
 {
+    constexpr int kUnr = 8;   // keys of each kind in flight per thread
     const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
     const int N = d.n;
-    k0i = order_key(a.key_imp[d.row_off]);
+    KeyStats r;
+    r.k0i = order_key(a.key_imp[d.row_off]);
     const uint32_t k0s = order_key(a.key_s[d.row_off]);
     uint32_t vi = 0, vs = 0, nlo = 0, hi = 0;
-    for (int i0 = tid; i0 < N; i0 += 4 * kThreads) {
-        float fi[4], fs[4];
+    for (int i0 = tid; i0 < N; i0 += kUnr * kThreads) {
+        float fi[kUnr], fs[kUnr];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
+        for (int u = 0; u < kUnr; ++u) {
             const int i = i0 + u * kThreads;
             if (i < N) {
                 fi[u] = a.key_imp[d.row_off + i];
@@ -194,13 +257,13 @@ __device__ void load_keys(const SelectArgs& a, const Img& d, uint32_t* ki, uint3
             }
         }
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
+        for (int u = 0; u < kUnr; ++u) {
             const int i = i0 + u * kThreads;
             if (i < N) {
                 const uint32_t qi = order_key(fi[u]), qs = order_key(fs[u]);
                 ki[i] = qi;
                 ks[i] = qs;
-                vi |= qi ^ k0i;
+                vi |= qi ^ r.k0i;
                 vs |= qs ^ k0s;
                 nlo = max(nlo, ~qi);
                 hi = max(hi, qi);
@@ -219,18 +282,45 @@ __device__ void load_keys(const SelectArgs& a, const Img& d, uint32_t* ki, uint3
         slots[3 * kW + w] = hi;
     }
     __syncthreads();
-    VI = 0;
-    VS = 0;
-    nlo = 0;
-    hi = 0;
-    for (int i = 0; i < kW; ++i) {
-        VI |= slots[i];
-        VS |= slots[kW + i];
-        nlo = max(nlo, slots[2 * kW + i]);
-        hi = max(hi, slots[3 * kW + i]);
+    r.VI = or_all(slots, lane);
+    r.VS = or_all(slots + kW, lane);
+    nlo = max_all(slots + 2 * kW, lane);
+    hi = max_all(slots + 3 * kW, lane);
+    r.kimin = ~nlo;
+    r.kimax = hi;
+    return r;
+}
+
+// Append (key, index) of the lanes with `member` set to `list`, reserving the
+// wavefront's slots with one atomic on the counter `cnt`.
+__device__ __forceinline__ void append_member(bool member, uint32_t key, int i, uint64_t* list,
+                                              uint32_t* cnt, int lane)
+{
+    const uint64_t bm = __ballot(member);
+    if (!bm) return;
+    const int leader = (int)__ffsll((long long)bm) - 1;
+    uint32_t b0 = 0;
+    if (lane == leader) b0 = atomicAdd(cnt, (uint32_t)__popcll(bm));
+    b0 = (uint32_t)__builtin_amdgcn_readlane((int)b0, leader);
+    if (member) list[b0 + __popcll(bm & lanes_below(lane))] = ((uint64_t)key << 16) | (uint32_t)i;
+}
+
+// Keep the `need` smallest of the m listed (key, index) members of the Stage I
+// boundary bucket: thread j counts the entries below entry j (the entries are
+// distinct, so the counts are the ranks) and sets the member's bits.
+__device__ void keep_ranked_members(const uint64_t* list, uint32_t m, uint32_t need, uint32_t* bimp,
+                                    uint32_t* bsel)
+{
+    const int tid = threadIdx.x;
+    if (tid >= (int)m) return;
+    const uint64_t mine = list[tid];
+    uint32_t r = 0;
+    for (uint32_t j = 0; j < m; ++j) r += list[j] < mine ? 1u : 0u;
+    if (r < need) {
+        const int i = (int)(mine & 0xffffu);
+        atomicOr(&bimp[i >> 5], 1u << (i & 31));
+        atomicOr(&bsel[i >> 5], 1u << (i & 31));
     }
-    kimin = ~nlo;
-    kimax = hi;
 }
 
 // Stage I digit passes (see the file comment).  On return the bucket
@@ -314,9 +404,14 @@ __device__ bool stage1_bucket(const uint32_t* ki, int N, uint32_t K1, uint32_t k
     const float width = key_value(kimax) - fmin;
     if (!(width > 0.f) || !(width < 3.0e38f)) return false;
     const float scale = (float)kBuckets / width;
-    for (int base = beg; base < end; base += kWave) {
-        const int i = base + lane;
-        if (i < end) atomicAdd(&H[value_bucket(ki[i], fmin, scale)], 1u);
+    for (int base = beg; base < end; base += kTileUnr * kWave) {
+        uint32_t k[kTileUnr];
+        load_tiles(ki, base, end, lane, k);
+#pragma unroll
+        for (int u = 0; u < kTileUnr; ++u) {
+            const int dg = value_bucket(k[u], fmin, scale);
+            if (base + u * kWave + lane < end) atomicAdd(&H[dg], 1u);
+        }
     }
     __syncthreads();
     {   // thread tid owns bucket tid: find the bucket holding the K1-th key
@@ -324,8 +419,7 @@ __device__ bool stage1_bucket(const uint32_t* ki, int N, uint32_t K1, uint32_t k
         const uint32_t inc = wave_scan_add(c);
         if (lane == kWave - 1) row[w] = inc;
         __syncthreads();
-        uint32_t start = inc - c;
-        for (int i = 0; i < w; ++i) start += row[i];
+        const uint32_t start = inc - c + sum_before(row, w, lane);
         if (start < K1 && K1 <= start + c) {
             misc[0] = (uint32_t)tid;
             misc[1] = K1 - start;
@@ -336,37 +430,24 @@ __device__ bool stage1_bucket(const uint32_t* ki, int N, uint32_t K1, uint32_t k
     const int dstar = (int)misc[0];
     const uint32_t need = misc[1];
     if (misc[2] > kCountLimit) return false;
-    for (int base = beg; base < end; base += kWave) {
-        const int i = base + lane;
-        const uint32_t key = i < end ? ki[i] : 0u;
-        const bool member = i < end && value_bucket(key, fmin, scale) == dstar;
-        const uint64_t bm = __ballot(member);
-        if (bm) {
-            const int leader = (int)__ffsll((long long)bm) - 1;
-            uint32_t b0 = 0;
-            if (lane == leader) b0 = atomicAdd(&misc[8], (uint32_t)__popcll(bm));
-            b0 = (uint32_t)__builtin_amdgcn_readlane((int)b0, leader);
-            if (member) list[b0 + __popcll(bm & lanes_below(lane))] = ((uint64_t)key << 16) | (uint32_t)i;
+    for (int base = beg; base < end; base += kTileUnr * kWave) {
+        uint32_t k[kTileUnr];
+        load_tiles(ki, base, end, lane, k);
+#pragma unroll
+        for (int u = 0; u < kTileUnr; ++u) {
+            const int tb = base + u * kWave;
+            if (tb >= end) break;   // the next tiles belong to the next wavefront
+            const int i = tb + lane;
+            const int dv = value_bucket(k[u], fmin, scale);
+            const int dg = i < end ? dv : kBuckets;
+            const uint64_t bt = __ballot(dg < dstar);
+            put_tile_bits(bimp, tb, bt, lane);
+            put_tile_bits(bsel, tb, bt, lane);
+            append_member(dg == dstar, k[u], i, list, &misc[8], lane);
         }
     }
     __syncthreads();
-    const uint32_t m = misc[8];
-    for (int base = beg; base < end; base += kWave) {
-        const int i = base + lane;
-        const bool act = i < end;
-        const uint32_t key = act ? ki[i] : 0u;
-        const int dg = act ? value_bucket(key, fmin, scale) : kBuckets;
-        bool take = act && dg < dstar;
-        if (act && dg == dstar) {
-            const uint64_t mine = ((uint64_t)key << 16) | (uint32_t)i;
-            uint32_t r = 0;
-            for (uint32_t j = 0; j < m; ++j) r += list[j] < mine ? 1u : 0u;
-            take = r < need;
-        }
-        const uint64_t bt = __ballot(take);
-        put_tile_bits(bimp, base, bt, lane);
-        put_tile_bits(bsel, base, bt, lane);
-    }
+    keep_ranked_members(list, misc[8], need, bimp, bsel);
     return true;
 }
 
@@ -413,44 +494,27 @@ __device__ void stage1_mark_counted(const uint32_t* ki, int N, uint32_t prefix, 
         const int i = base + lane;
         const bool act = i < end;
         const uint32_t key = act ? ki[i] : 0u;
-        const bool member = act && (key & pmask) == prefix;
-        const uint64_t bm = __ballot(member);
-        if (bm) {
-            const int leader = (int)__ffsll((long long)bm) - 1;
-            uint32_t b0 = 0;
-            if (lane == leader) b0 = atomicAdd(&misc[8], (uint32_t)__popcll(bm));
-            b0 = (uint32_t)__builtin_amdgcn_readlane((int)b0, leader);
-            if (member) list[b0 + __popcll(bm & lanes_below(lane))] = ((uint64_t)key << 16) | (uint32_t)i;
-        }
-    }
-    __syncthreads();
-    const uint32_t m = misc[8];
-    for (int base = beg; base < end; base += kWave) {
-        const int i = base + lane;
-        const bool act = i < end;
-        const uint32_t key = act ? ki[i] : 0u;
-        const bool member = act && (key & pmask) == prefix;
-        const bool below = act && (key & pmask) < prefix;
-        uint32_t r = 0;
-        if (member) {
-            const uint64_t mine = ((uint64_t)key << 16) | (uint32_t)i;
-            for (uint32_t j = 0; j < m; ++j) r += list[j] < mine ? 1u : 0u;
-        }
-        const uint64_t bt = __ballot(below || (member && r < need));
+        const uint64_t bt = __ballot(act && (key & pmask) < prefix);
         put_tile_bits(bimp, base, bt, lane);
         put_tile_bits(bsel, base, bt, lane);
+        append_member(act && (key & pmask) == prefix, key, i, list, &misc[8], lane);
     }
+    __syncthreads();
+    keep_ranked_members(list, misc[8], need, bimp, bsel);
 }
 
 // Stage II by one bucketing pass and exact counting inside buckets.  Bucket
 // d of a remaining token is floor((s - s_min) * B / (s_max - s_min)) (B =
-// 1024 buckets over the remainder's key range), a non-decreasing function of s
+// 1024 buckets over the remainder's key range: the image's whole range would
+// be cheaper to get, but Stage I tends to keep the tokens with outlying keys
+// and the rest would crowd into few buckets), a non-decreasing function of s
 // in fp32 (every step rounds monotonically), so bucket order agrees with key
 // order and counting inside a bucket the members smaller in (key, index)
-// order gives the exact rank.  `list` receives the indices of X^rem in bucket
-// order (n u16).  H (B words) must be zero.  Returns false, having written
-// only H, cur, list and slot rows, when a bucket holds more than kBucketLimit
-// tokens or the key range is not finite.
+// order gives the exact rank.  `list` receives the indices of X^rem in bucket order
+// (n u16); with `parts` workgroups on a dense image each lists only the
+// buckets it ranks.  H (B words) must be zero.  Returns kS2Failed, having
+// written only H, cur, list and slot rows, when a bucket holds more than
+// kBucketLimit tokens or the key range is not finite.
 // X^div positions in the ascending order of X^rem (R tokens, K2 picks).
 // Algorithm 1: 0, t, ..., (K2 - 1) t.  Real-interval variant (the interval
 // R / K2 of the method's prose): floor(j R / K2), j < K2.  Every product
@@ -476,8 +540,8 @@ constexpr int kS2Global = 2;   // this group's picks are in the global bitmap
 
 __device__ int stage2_bucket(const uint32_t* ks, const uint32_t* bimp, uint32_t* bsel, int N,
                               int R, const Stride& sp, uint32_t* H, uint32_t* cur, uint16_t* list,
-                              uint32_t* row_lo, uint32_t* row_hi, uint32_t* row_a, uint32_t* row_b,
-                              int part, int parts, uint32_t* gpick)
+                              uint32_t* pairs, uint32_t* row_lo, uint32_t* row_hi, uint32_t* row_a,
+                              uint32_t* row_b, int part, int parts, uint32_t* gpick)
 {
     const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
     int beg, end;
@@ -485,11 +549,17 @@ __device__ int stage2_bucket(const uint32_t* ks, const uint32_t* bimp, uint32_t*
 
     // key range of X^rem (max of the complement gives the minimum)
     uint32_t nlo = 0, hi = 0;
-    for (int base = beg; base < end; base += kWave) {
-        const int i = base + lane;
-        if (i < end && !bit_of(bimp, i)) {
-            nlo = max(nlo, ~ks[i]);
-            hi = max(hi, ks[i]);
+    for (int base = beg; base < end; base += kTileUnr * kWave) {
+        uint32_t k[kTileUnr];
+        bool rem[kTileUnr];
+        load_tiles(ks, base, end, lane, k);
+        rem_tiles(bimp, base, end, lane, rem);
+#pragma unroll
+        for (int u = 0; u < kTileUnr; ++u) {
+            if (rem[u]) {
+                nlo = max(nlo, ~k[u]);
+                hi = max(hi, k[u]);
+            }
         }
     }
     nlo = wave_max_u32(nlo);
@@ -499,12 +569,7 @@ __device__ int stage2_bucket(const uint32_t* ks, const uint32_t* bimp, uint32_t*
         row_hi[w] = hi;
     }
     __syncthreads();
-    uint32_t kmin = 0, kmax = 0;
-    for (int i = 0; i < kW; ++i) {
-        kmin = max(kmin, row_lo[i]);
-        kmax = max(kmax, row_hi[i]);
-    }
-    kmin = ~kmin;
+    const uint32_t kmin = ~max_all(row_lo, lane), kmax = max_all(row_hi, lane);
 
     if (kmin == kmax) {
         // Every remaining key is equal: the stable order is the token order of X^rem.
@@ -520,8 +585,7 @@ __device__ int stage2_bucket(const uint32_t* ks, const uint32_t* bimp, uint32_t*
             const uint64_t br = __ballot(rem);
             const uint32_t r = r0 + (uint32_t)__popcll(br & lanes_below(lane));
             const uint64_t bp = __ballot(rem && sp.picks(r));
-            if (lane == 0) bsel[base >> 5] = bimp[base >> 5] | (uint32_t)bp;
-            if (lane == 32) bsel[(base >> 5) + 1] = bimp[(base >> 5) + 1] | (uint32_t)(bp >> 32);
+            put_tile_union(bsel, bimp, base, bp, lane);
             r0 += (uint32_t)__popcll(br);
         }
         return kS2Local;
@@ -531,11 +595,15 @@ __device__ int stage2_bucket(const uint32_t* ks, const uint32_t* bimp, uint32_t*
     if (!(width > 0.f) || !(width < 3.0e38f)) return kS2Failed;   // not finite: sort instead
     const float scale = (float)kBuckets / width;
 
-    for (int base = beg; base < end; base += kWave) {
-        const int i = base + lane;
-        if (i < end && !bit_of(bimp, i)) {
-            const int dg = value_bucket(ks[i], fmin, scale);
-            atomicAdd(&H[dg], 1u);
+    for (int base = beg; base < end; base += kTileUnr * kWave) {
+        uint32_t k[kTileUnr];
+        bool rem[kTileUnr];
+        load_tiles(ks, base, end, lane, k);
+        rem_tiles(bimp, base, end, lane, rem);
+#pragma unroll
+        for (int u = 0; u < kTileUnr; ++u) {
+            const int dg = value_bucket(k[u], fmin, scale);
+            if (rem[u]) atomicAdd(&H[dg], 1u);
         }
     }
     __syncthreads();
@@ -546,32 +614,45 @@ __device__ int stage2_bucket(const uint32_t* ks, const uint32_t* bimp, uint32_t*
         if (lane == kWave - 1) row_a[w] = inc;
         if (lane == 0) row_b[w] = mx;
         __syncthreads();
-        uint32_t start = inc - c, big = 0;
-        for (int i = 0; i < kW; ++i) {
-            if (i < w) start += row_a[i];
-            big = max(big, row_b[i]);
-        }
+        const uint32_t start = inc - c + sum_before(row_a, w, lane);
+        const uint32_t big = max_all(row_b, lane);
         cur[tid] = start;
         if (big > kBucketLimit) return kS2Failed;   // the same decision in every thread
     }
     __syncthreads();
-    for (int base = beg; base < end; base += kWave) {
-        const int i = base + lane;
-        if (i < end && !bit_of(bimp, i)) {
-            const int dg = value_bucket(ks[i], fmin, scale);
-            list[atomicAdd(&cur[dg], 1u)] = (uint16_t)i;
+    // Dense ranking gives bucket q to wavefront q % (parts W) across the
+    // groups, so to group (q / W) % parts (parts is 1 or a power of two).
+    const bool dense = R >= kDenseRem;
+    for (int base = beg; base < end; base += kTileUnr * kWave) {
+        uint32_t k[kTileUnr];
+        bool rem[kTileUnr];
+        load_tiles(ks, base, end, lane, k);
+        rem_tiles(bimp, base, end, lane, rem);
+#pragma unroll
+        for (int u = 0; u < kTileUnr; ++u) {   // all cursor atomics, then the stores
+            const int dg = value_bucket(k[u], fmin, scale);
+            rem[u] = rem[u] && (!dense || ((dg / kW) & (parts - 1)) == part);
+            if (rem[u]) k[u] = atomicAdd(&cur[dg], 1u);
         }
+#pragma unroll
+        for (int u = 0; u < kTileUnr; ++u)
+            if (rem[u]) list[k[u]] = (uint16_t)(base + u * kWave + lane);
     }
     __syncthreads();
-    if (R >= kDenseRem) {
+    if (dense) {
         // Dense buckets: a wavefront ranks a whole bucket at a time.  Members
         // sit in lanes (64 per chunk) and every member of the bucket is
         // broadcast from its lane, so each member is read from LDS once.
         // With `parts` workgroups on the image, bucket q belongs to the
         // wavefront numbered q % (parts W) across them (lane q / (parts W));
         // picks then go to the image's global bitmap gpick.
-        const int waves = parts * kW;
-        const int q = part * kW + w + waves * lane;
+        // A chunk of up to 64 members is staged as (index, key) word pairs
+        // in the wavefront's own `pairs` row, where every lane reads each
+        // pair with one broadcast LDS read and compares (key, index) as one
+        // 64-bit value.  LDS operations of one wavefront complete in order,
+        // so a pair written by any lane is visible to the reads after it.
+        uint32_t* wp = pairs + 2 * kWave * w;
+        const int q = part * kW + w + parts * kW * lane;
         const bool mine = q < kBuckets;
         const uint32_t cnt = mine ? H[q] : 0u;
         const uint32_t stop = mine ? cur[q] : 0u;
@@ -584,20 +665,29 @@ __device__ int stage2_bucket(const uint32_t* ks, const uint32_t* bimp, uint32_t*
             for (uint32_t c0 = 0; c0 < b; c0 += kWave) {
                 const bool have = c0 + lane < b;
                 const uint32_t myid = have ? list[start + c0 + lane] : 0u;
-                const uint32_t mykey = have ? ks[myid] : 0u;
+                const uint64_t me = have ? ((uint64_t)ks[myid] << 32) | myid : 0ull;
                 uint32_t r = 0;
                 for (uint32_t c1 = 0; c1 < b; c1 += kWave) {
-                    uint32_t oid = myid, okey = mykey;
-                    if (c1 != c0) {
-                        const bool oh = c1 + lane < b;
-                        oid = oh ? list[start + c1 + lane] : 0u;
-                        okey = oh ? ks[oid] : 0u;
-                    }
+                    const bool oh = c1 + lane < b;
+                    const uint32_t oid = oh ? list[start + c1 + lane] : 0u;
+                    const uint32_t okey = oh ? ks[oid] : 0u;
+                    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+                    wp[2 * lane] = oid;
+                    wp[2 * lane + 1] = okey;
+                    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
                     const uint32_t n1 = min((uint32_t)kWave, b - c1);
-                    for (uint32_t j = 0; j < n1; ++j) {
-                        const uint32_t kj = (uint32_t)__builtin_amdgcn_readlane((int)okey, (int)j);
-                        const uint32_t ij = (uint32_t)__builtin_amdgcn_readlane((int)oid, (int)j);
-                        r += (kj < mykey || (kj == mykey && ij < myid)) ? 1u : 0u;
+                    uint32_t j = 0;
+                    for (; j + 4 <= n1; j += 4) {   // four reads in flight
+                        uint64_t o[4];
+#pragma unroll
+                        for (int u = 0; u < 4; ++u)
+                            o[u] = ((uint64_t)wp[2 * (j + u) + 1] << 32) | wp[2 * (j + u)];
+#pragma unroll
+                        for (int u = 0; u < 4; ++u) r += o[u] < me ? 1u : 0u;
+                    }
+                    for (; j < n1; ++j) {
+                        const uint64_t o = ((uint64_t)wp[2 * j + 1] << 32) | wp[2 * j];
+                        r += o < me ? 1u : 0u;
                     }
                 }
                 const uint32_t rr = start + r;
@@ -634,8 +724,7 @@ __device__ int stage2_bucket(const uint32_t* ks, const uint32_t* bimp, uint32_t*
             picked = sp.picks(r);
         }
         const uint64_t bp = __ballot(picked);
-        if (lane == 0) bsel[base >> 5] = bimp[base >> 5] | (uint32_t)bp;
-        if (lane == 32) bsel[(base >> 5) + 1] = bimp[(base >> 5) + 1] | (uint32_t)(bp >> 32);
+        put_tile_union(bsel, bimp, base, bp, lane);
     }
     return kS2Local;
 }
@@ -689,8 +778,7 @@ __device__ void stage2_radix(const uint32_t* ks, const uint32_t* bimp, uint32_t*
             const uint32_t inc = wave_scan_add(v);
             if (lane == kWave - 1) row_s[w] = inc;
             __syncthreads();
-            uint32_t b0 = inc - v;
-            for (int i = 0; i < w; ++i) b0 += row_s[i];
+            const uint32_t b0 = inc - v + sum_before(row_s, w, lane);
             const uint32_t o1 = b0 + h0, o2 = o1 + h1, o3 = o2 + h2;
             *reinterpret_cast<uint2*>(hist + e) = make_uint2(b0 | (o1 << 16), o2 | (o3 << 16));
         }
@@ -773,9 +861,9 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a)
     // again until further barriers have passed): 0-3 key ranges and varying
     // bits, 4 Stage I scans, 5 Stage I tie ranks, 6-7 Stage II ranges, 2-3
     // Stage II scans, 4-5 the radix sort, 6 the output offsets.
-    uint32_t k0i, VI, VS, kimin, kimax;
     if (threadIdx.x < 16) misc[threadIdx.x] = 0;
-    load_keys(a, d, ki, ks, area, kBuckets, slots, k0i, VI, VS, kimin, kimax);
+    const KeyStats ksd = load_keys(a, d, ki, ks, area, kBuckets, slots);
+    const uint32_t kimin = ksd.kimin, kimax = ksd.kimax;
 
     // ---- Stage I ---------------------------------------------------------------
     uint64_t* list1 = reinterpret_cast<uint64_t*>(area + kBuckets);   // kCountLimit u64
@@ -793,9 +881,9 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a)
         area[threadIdx.x] = 0;
         if (threadIdx.x < 16) misc[threadIdx.x] = 0;
         __syncthreads();
-        uint32_t prefix = k0i & ~VI, pmask = ~VI, need = (uint32_t)K1, m = (uint32_t)N;
+        uint32_t prefix = ksd.k0i & ~ksd.VI, pmask = ~ksd.VI, need = (uint32_t)K1, m = (uint32_t)N;
         bool resolved;
-        stage1_narrow(ki, N, VI, area, misc, kCountLimit, prefix, pmask, need, m, resolved);
+        stage1_narrow(ki, N, ksd.VI, area, misc, kCountLimit, prefix, pmask, need, m, resolved);
         if (resolved) stage1_mark_resolved(ki, N, prefix, need, bimp, bsel, slots + 5 * kW);
         else stage1_mark_counted(ki, N, prefix, pmask, need, list1, misc, bimp, bsel);
     }
@@ -809,13 +897,16 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a)
         const size_t wbase = (size_t)(d.row_off >> 5) + 2 * (size_t)img;
         uint32_t* gpick = split ? a.gsel + wbase : nullptr;
         const Stride sp{(uint32_t)d.t, (uint32_t)(N - K1), (uint32_t)K2, a.stride_real != 0};
+        // Dense ranking stages pairs in the upper half of ki's bytes, above
+        // the u16 list of X^rem: room for 2 kWave words per wavefront once
+        // N >= kDenseRem.
         int st = stage2_bucket(ks, bimp, bsel, N, N - K1, sp, area, area + kBuckets, idx,
-                               slots + 6 * kW, slots + 7 * kW, slots + 2 * kW, slots + 3 * kW,
-                               split ? part : 0, split ? G : 1, gpick);
+                               ki + (N + 1) / 2, slots + 6 * kW, slots + 7 * kW, slots + 2 * kW,
+                               slots + 3 * kW, split ? part : 0, split ? G : 1, gpick);
         if (st == kS2Failed) {
             if (part > 0) return;   // the same decision in every group: group 0 sorts
             __syncthreads();        // every thread is past the bucket attempt
-            stage2_radix(ks, bimp, bsel, N, K1, sp, VS, idx, idx + N,
+            stage2_radix(ks, bimp, bsel, N, K1, sp, ksd.VS, idx, idx + N,
                          reinterpret_cast<uint16_t*>(area), slots + 4 * kW, slots + 5 * kW);
             st = kS2Local;
         }

@@ -174,6 +174,12 @@ def _select_cases(rng, trials=60):
     cases.append(([18432], [1152], 1 / 3))
     cases.append(([65] * 40, [13] * 40, 1 / 3))                       # > 32 images, uniform
     cases.append(([65, 70] * 20, [13, 14] * 20, 1 / 3))               # > 32 images, ragged
+    # the smallest remainders ranked bucket-by-bucket across split groups
+    # (R = N - K1 >= 4096): the per-wavefront staging rows fill the LDS
+    # above the remainder list exactly at N = 4096
+    cases.append(([4096], [512], 0.0))
+    cases.append(([4097, 4099, 4096], [3, 700, 4096], 0.0))
+    cases.append(([4098], [6], 1 / 3))
     # key shapes that steer the selection's internal paths: all keys equal,
     # one outlier that puts every other key in one bucket, narrow clusters
     shaped = []
