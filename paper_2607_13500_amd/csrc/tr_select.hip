@@ -42,7 +42,9 @@ constexpr int kBuckets = kThreads;       // Stage II: value buckets (one per thr
 constexpr uint32_t kBucketLimit = 256;   // Stage II: largest bucket ranked by counting
 constexpr int kDenseRem = 4096;          // Stage II: rank whole buckets per wavefront from here
 constexpr int kSplitGroups = 16;         // workgroups sharing the ranking of one large image
-static_assert(kCountLimit <= (uint32_t)kThreads, "one thread per listed Stage I member");
+constexpr uint16_t kNoBucket = 0xffff;   // Stage II bucket index of a token not in X^rem
+static_assert(kCountLimit <= (uint32_t)kThreads && kCountLimit % kWave == 0,
+              "one thread per listed Stage I member, in whole wavefronts");
 static_assert((kSplitGroups & (kSplitGroups - 1)) == 0, "split ownership is a mask");
 static_assert(kDenseRem / 2 >= 2 * kWave * kW, "dense ranking's pairs fit above the X^rem list");
 
@@ -307,19 +309,35 @@ __device__ __forceinline__ void append_member(bool member, uint32_t key, int i, 
 
 // Keep the `need` smallest of the m listed (key, index) members of the Stage I
 // boundary bucket: thread j counts the entries below entry j (the entries are
-// distinct, so the counts are the ranks) and sets the member's bits.
+// distinct, so the counts are the ranks) and sets the member's bits.  With ks
+// given, the Stage II keys of the members left in X^rem are folded into the
+// per-wavefront range rows (~min, max) of wavefronts 0 and 1.
 __device__ void keep_ranked_members(const uint64_t* list, uint32_t m, uint32_t need, uint32_t* bimp,
-                                    uint32_t* bsel)
+                                    uint32_t* bsel, const uint32_t* ks, uint32_t* row_lo,
+                                    uint32_t* row_hi)
 {
-    const int tid = threadIdx.x;
-    if (tid >= (int)m) return;
-    const uint64_t mine = list[tid];
-    uint32_t r = 0;
-    for (uint32_t j = 0; j < m; ++j) r += list[j] < mine ? 1u : 0u;
-    if (r < need) {
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
+    uint32_t nlo = 0, hi = 0;
+    if (tid < (int)m) {
+        const uint64_t mine = list[tid];
+        uint32_t r = 0;
+        for (uint32_t j = 0; j < m; ++j) r += list[j] < mine ? 1u : 0u;
         const int i = (int)(mine & 0xffffu);
-        atomicOr(&bimp[i >> 5], 1u << (i & 31));
-        atomicOr(&bsel[i >> 5], 1u << (i & 31));
+        if (r < need) {
+            atomicOr(&bimp[i >> 5], 1u << (i & 31));
+            atomicOr(&bsel[i >> 5], 1u << (i & 31));
+        } else if (ks) {
+            nlo = ~ks[i];
+            hi = ks[i];
+        }
+    }
+    if (ks && tid < (int)kCountLimit) {   // whole wavefronts: every lane takes part
+        nlo = wave_max_u32(nlo);
+        hi = wave_max_u32(hi);
+        if (lane == 0) {
+            row_lo[w] = max(row_lo[w], nlo);
+            row_hi[w] = max(row_hi[w], hi);
+        }
     }
 }
 
@@ -391,10 +409,13 @@ __device__ __forceinline__ int value_bucket(uint32_t key, float fmin, float scal
 // members of that bucket (at most kCountLimit of them) are kept when fewer
 // than the remaining budget of members precede them in (key, index) order.
 // H (kBuckets words) must be zero; list holds kCountLimit u64; misc[8] must be
-// 0.  Returns false (having written only H, misc[0..2] and `row`) when the
-// range is not finite or the boundary bucket is larger.
-__device__ bool stage1_bucket(const uint32_t* ki, int N, uint32_t K1, uint32_t kimin, uint32_t kimax,
-                              uint32_t* H, uint64_t* list, uint32_t* misc, uint32_t* row,
+// 0.  On success row_lo / row_hi hold per-wavefront (~min, max) of the Stage II
+// keys of X^rem, so Stage II needs no range pass of its own.  Returns false
+// (having written only H, misc[0..2] and `row`) when the range is not finite
+// or the boundary bucket is larger.
+__device__ bool stage1_bucket(const uint32_t* ki, const uint32_t* ks, int N, uint32_t K1,
+                              uint32_t kimin, uint32_t kimax, uint32_t* H, uint64_t* list,
+                              uint32_t* misc, uint32_t* row, uint32_t* row_lo, uint32_t* row_hi,
                               uint32_t* bimp, uint32_t* bsel)
 {
     const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
@@ -430,9 +451,11 @@ __device__ bool stage1_bucket(const uint32_t* ki, int N, uint32_t K1, uint32_t k
     const int dstar = (int)misc[0];
     const uint32_t need = misc[1];
     if (misc[2] > kCountLimit) return false;
+    uint32_t nlo = 0, hi = 0;   // Stage II key range of the tokens above the boundary bucket
     for (int base = beg; base < end; base += kTileUnr * kWave) {
-        uint32_t k[kTileUnr];
+        uint32_t k[kTileUnr], q[kTileUnr];
         load_tiles(ki, base, end, lane, k);
+        load_tiles(ks, base, end, lane, q);
 #pragma unroll
         for (int u = 0; u < kTileUnr; ++u) {
             const int tb = base + u * kWave;
@@ -444,10 +467,19 @@ __device__ bool stage1_bucket(const uint32_t* ki, int N, uint32_t K1, uint32_t k
             put_tile_bits(bimp, tb, bt, lane);
             put_tile_bits(bsel, tb, bt, lane);
             append_member(dg == dstar, k[u], i, list, &misc[8], lane);
+            const bool above = i < end && dg > dstar;
+            nlo = max(nlo, above ? ~q[u] : 0u);
+            hi = max(hi, above ? q[u] : 0u);
         }
     }
+    nlo = wave_max_u32(nlo);
+    hi = wave_max_u32(hi);
+    if (lane == 0) {
+        row_lo[w] = nlo;
+        row_hi[w] = hi;
+    }
     __syncthreads();
-    keep_ranked_members(list, misc[8], need, bimp, bsel);
+    keep_ranked_members(list, misc[8], need, bimp, bsel, ks, row_lo, row_hi);
     return true;
 }
 
@@ -500,21 +532,9 @@ __device__ void stage1_mark_counted(const uint32_t* ki, int N, uint32_t prefix, 
         append_member(act && (key & pmask) == prefix, key, i, list, &misc[8], lane);
     }
     __syncthreads();
-    keep_ranked_members(list, misc[8], need, bimp, bsel);
+    keep_ranked_members(list, misc[8], need, bimp, bsel, nullptr, nullptr, nullptr);
 }
 
-// Stage II by one bucketing pass and exact counting inside buckets.  Bucket
-// d of a remaining token is floor((s - s_min) * B / (s_max - s_min)) (B =
-// 1024 buckets over the remainder's key range: the image's whole range would
-// be cheaper to get, but Stage I tends to keep the tokens with outlying keys
-// and the rest would crowd into few buckets), a non-decreasing function of s
-// in fp32 (every step rounds monotonically), so bucket order agrees with key
-// order and counting inside a bucket the members smaller in (key, index)
-// order gives the exact rank.  `list` receives the indices of X^rem in bucket order
-// (n u16); with `parts` workgroups on a dense image each lists only the
-// buckets it ranks.  H (B words) must be zero.  Returns kS2Failed, having
-// written only H, cur, list and slot rows, when a bucket holds more than
-// kBucketLimit tokens or the key range is not finite.
 // X^div positions in the ascending order of X^rem (R tokens, K2 picks).
 // Algorithm 1: 0, t, ..., (K2 - 1) t.  Real-interval variant (the interval
 // R / K2 of the method's prose): floor(j R / K2), j < K2.  Every product
@@ -538,37 +558,59 @@ constexpr int kS2Failed = 0;   // nothing decided: sort instead
 constexpr int kS2Local = 1;    // every pick is in bsel
 constexpr int kS2Global = 2;   // this group's picks are in the global bitmap
 
+// Stage II by one bucketing pass and exact counting inside buckets.  Bucket
+// d of a remaining token is floor((s - s_min) * B / (s_max - s_min)) (B =
+// 1024 buckets over the remainder's key range: the image's whole range would
+// be cheaper to get, but Stage I tends to keep the tokens with outlying keys
+// and the rest would crowd into few buckets), a non-decreasing function of s
+// in fp32 (every step rounds monotonically), so bucket order agrees with key
+// order and counting inside a bucket the members smaller in (key, index)
+// order gives the exact rank.
+//   dgs   u16[n]  each token's bucket (kNoBucket outside X^rem), written by
+//                 the histogram pass, read by the list pass
+//   list  u16[n]  the indices of X^rem in bucket order; with `parts`
+//                 workgroups on a dense image each lists only the buckets it
+//                 ranks
+//   pairs         2 kWave words per wavefront for the dense ranking (may
+//                 overlap dgs, which is dead by then)
+// H (B words) must be zero.  Returns kS2Failed, having written only H, cur,
+// dgs, list and slot rows, when a bucket holds more than kBucketLimit tokens
+// or the key range is not finite.
 __device__ int stage2_bucket(const uint32_t* ks, const uint32_t* bimp, uint32_t* bsel, int N,
                               int R, const Stride& sp, uint32_t* H, uint32_t* cur, uint16_t* list,
-                              uint32_t* pairs, uint32_t* row_lo, uint32_t* row_hi, uint32_t* row_a,
-                              uint32_t* row_b, int part, int parts, uint32_t* gpick)
+                              uint16_t* dgs, uint32_t* pairs, uint32_t* row_lo, uint32_t* row_hi,
+                              uint32_t* row_a, uint32_t* row_b, int part, int parts,
+                              uint32_t* gpick, bool have_range)
 {
     const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
     int beg, end;
     wave_range(N, w, beg, end);
 
-    // key range of X^rem (max of the complement gives the minimum)
-    uint32_t nlo = 0, hi = 0;
-    for (int base = beg; base < end; base += kTileUnr * kWave) {
-        uint32_t k[kTileUnr];
-        bool rem[kTileUnr];
-        load_tiles(ks, base, end, lane, k);
-        rem_tiles(bimp, base, end, lane, rem);
+    // key range of X^rem (max of the complement gives the minimum), unless
+    // Stage I left it in the rows (the same decision in every thread)
+    if (!have_range) {
+        uint32_t nlo = 0, hi = 0;
+        for (int base = beg; base < end; base += kTileUnr * kWave) {
+            uint32_t k[kTileUnr];
+            bool rem[kTileUnr];
+            load_tiles(ks, base, end, lane, k);
+            rem_tiles(bimp, base, end, lane, rem);
 #pragma unroll
-        for (int u = 0; u < kTileUnr; ++u) {
-            if (rem[u]) {
-                nlo = max(nlo, ~k[u]);
-                hi = max(hi, k[u]);
+            for (int u = 0; u < kTileUnr; ++u) {
+                if (rem[u]) {
+                    nlo = max(nlo, ~k[u]);
+                    hi = max(hi, k[u]);
+                }
             }
         }
+        nlo = wave_max_u32(nlo);
+        hi = wave_max_u32(hi);
+        if (lane == 0) {
+            row_lo[w] = nlo;
+            row_hi[w] = hi;
+        }
+        __syncthreads();
     }
-    nlo = wave_max_u32(nlo);
-    hi = wave_max_u32(hi);
-    if (lane == 0) {
-        row_lo[w] = nlo;
-        row_hi[w] = hi;
-    }
-    __syncthreads();
     const uint32_t kmin = ~max_all(row_lo, lane), kmax = max_all(row_hi, lane);
 
     if (kmin == kmax) {
@@ -602,8 +644,10 @@ __device__ int stage2_bucket(const uint32_t* ks, const uint32_t* bimp, uint32_t*
         rem_tiles(bimp, base, end, lane, rem);
 #pragma unroll
         for (int u = 0; u < kTileUnr; ++u) {
+            const int i = base + u * kWave + lane;
             const int dg = value_bucket(k[u], fmin, scale);
             if (rem[u]) atomicAdd(&H[dg], 1u);
+            if (i < end) dgs[i] = rem[u] ? (uint16_t)dg : kNoBucket;
         }
     }
     __syncthreads();
@@ -624,33 +668,34 @@ __device__ int stage2_bucket(const uint32_t* ks, const uint32_t* bimp, uint32_t*
     // groups, so to group (q / W) % parts (parts is 1 or a power of two).
     const bool dense = R >= kDenseRem;
     for (int base = beg; base < end; base += kTileUnr * kWave) {
-        uint32_t k[kTileUnr];
-        bool rem[kTileUnr];
-        load_tiles(ks, base, end, lane, k);
-        rem_tiles(bimp, base, end, lane, rem);
+        uint32_t g[kTileUnr];
+        bool own[kTileUnr];
+#pragma unroll
+        for (int u = 0; u < kTileUnr; ++u) {
+            const int i = base + u * kWave + lane;
+            g[u] = i < end ? dgs[i] : kNoBucket;
+        }
 #pragma unroll
         for (int u = 0; u < kTileUnr; ++u) {   // all cursor atomics, then the stores
-            const int dg = value_bucket(k[u], fmin, scale);
-            rem[u] = rem[u] && (!dense || ((dg / kW) & (parts - 1)) == part);
-            if (rem[u]) k[u] = atomicAdd(&cur[dg], 1u);
+            own[u] = g[u] != kNoBucket && (!dense || ((g[u] / kW) & (parts - 1)) == (uint32_t)part);
+            if (own[u]) g[u] = atomicAdd(&cur[g[u]], 1u);
         }
 #pragma unroll
         for (int u = 0; u < kTileUnr; ++u)
-            if (rem[u]) list[k[u]] = (uint16_t)(base + u * kWave + lane);
+            if (own[u]) list[g[u]] = (uint16_t)(base + u * kWave + lane);
     }
     __syncthreads();
     if (dense) {
-        // Dense buckets: a wavefront ranks a whole bucket at a time.  Members
-        // sit in lanes (64 per chunk) and every member of the bucket is
-        // broadcast from its lane, so each member is read from LDS once.
-        // With `parts` workgroups on the image, bucket q belongs to the
-        // wavefront numbered q % (parts W) across them (lane q / (parts W));
-        // picks then go to the image's global bitmap gpick.
-        // A chunk of up to 64 members is staged as (index, key) word pairs
-        // in the wavefront's own `pairs` row, where every lane reads each
-        // pair with one broadcast LDS read and compares (key, index) as one
-        // 64-bit value.  LDS operations of one wavefront complete in order,
-        // so a pair written by any lane is visible to the reads after it.
+        // Dense buckets: a wavefront ranks a whole bucket at a time, one
+        // member per lane (64 per chunk).  Each chunk of the bucket is
+        // staged as (index, key) word pairs in the wavefront's own `pairs`
+        // row, where every lane reads each pair with one broadcast LDS read
+        // and compares (key, index) as one 64-bit value.  LDS operations of
+        // one wavefront complete in order, so a pair written by any lane is
+        // visible to the reads after it.  With `parts` workgroups on the
+        // image, bucket q belongs to the wavefront numbered q % (parts W)
+        // across them (lane q / (parts W)); picks then go to the image's
+        // global pick bitmap gpick.
         uint32_t* wp = pairs + 2 * kWave * w;
         const int q = part * kW + w + parts * kW * lane;
         const bool mine = q < kBuckets;
@@ -859,14 +904,16 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a)
 
     // Slot rows (each written, then read after a barrier, then not touched
     // again until further barriers have passed): 0-3 key ranges and varying
-    // bits, 4 Stage I scans, 5 Stage I tie ranks, 6-7 Stage II ranges, 2-3
-    // Stage II scans, 4-5 the radix sort, 6 the output offsets.
+    // bits, 4 Stage I scans, 5 Stage I tie ranks, 6-7 Stage II ranges (from
+    // Stage I's bucket path or Stage II's own pass), 2-3 Stage II scans, 4-5
+    // the radix sort, 6 the output offsets.
     if (threadIdx.x < 16) misc[threadIdx.x] = 0;
     const KeyStats ksd = load_keys(a, d, ki, ks, area, kBuckets, slots);
     const uint32_t kimin = ksd.kimin, kimax = ksd.kimax;
 
     // ---- Stage I ---------------------------------------------------------------
     uint64_t* list1 = reinterpret_cast<uint64_t*>(area + kBuckets);   // kCountLimit u64
+    bool s2_range = false;   // Stage I's bucket path leaves X^rem's key range in rows 6-7
     if (K1 == 0 || K1 == N) {
         const uint32_t fill = K1 ? 0xffffffffu : 0u;
         for (int i = threadIdx.x; i < nw; i += kThreads) {
@@ -875,8 +922,10 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a)
         }
     } else if (kimin == kimax) {   // every key is equal: the first K1 tokens
         stage1_mark_resolved(ki, N, kimin, (uint32_t)K1, bimp, bsel, slots + 5 * kW);
-    } else if (!stage1_bucket(ki, N, (uint32_t)K1, kimin, kimax, area, list1, misc, slots + 4 * kW,
-                              bimp, bsel)) {
+    } else if (stage1_bucket(ki, ks, N, (uint32_t)K1, kimin, kimax, area, list1, misc, slots + 4 * kW,
+                             slots + 6 * kW, slots + 7 * kW, bimp, bsel)) {
+        s2_range = true;
+    } else {
         __syncthreads();   // everyone is past the bucket attempt: reset its scratch
         area[threadIdx.x] = 0;
         if (threadIdx.x < 16) misc[threadIdx.x] = 0;
@@ -897,12 +946,13 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a)
         const size_t wbase = (size_t)(d.row_off >> 5) + 2 * (size_t)img;
         uint32_t* gpick = split ? a.gsel + wbase : nullptr;
         const Stride sp{(uint32_t)d.t, (uint32_t)(N - K1), (uint32_t)K2, a.stride_real != 0};
-        // Dense ranking stages pairs in the upper half of ki's bytes, above
-        // the u16 list of X^rem: room for 2 kWave words per wavefront once
-        // N >= kDenseRem.
-        int st = stage2_bucket(ks, bimp, bsel, N, N - K1, sp, area, area + kBuckets, idx,
+        // ki's bytes after Stage I: the u16 list of X^rem in the lower half;
+        // the u16 bucket index of every token in the upper half (until the
+        // list is built); then the dense ranking's pairs above the list, with
+        // room for 2 kWave words per wavefront once N >= kDenseRem.
+        int st = stage2_bucket(ks, bimp, bsel, N, N - K1, sp, area, area + kBuckets, idx, idx + N,
                                ki + (N + 1) / 2, slots + 6 * kW, slots + 7 * kW, slots + 2 * kW,
-                               slots + 3 * kW, split ? part : 0, split ? G : 1, gpick);
+                               slots + 3 * kW, split ? part : 0, split ? G : 1, gpick, s2_range);
         if (st == kS2Failed) {
             if (part > 0) return;   // the same decision in every group: group 0 sorts
             __syncthreads();        // every thread is past the bucket attempt
