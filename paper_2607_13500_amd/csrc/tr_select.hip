@@ -7,24 +7,31 @@
 // 0, t, ..., (K2-1) t (or floor(j R / K2) in the real-interval variant); the
 // output lists X^imp U X^div in token order.
 //
-// Stage I narrows a bucket {k : (k & pmask) == prefix} that contains the K1-th
-// smallest key with 8-bit digit passes over the highest still-undecided bits
-// in which some key differs (bytes no key varies in cost nothing).  Each pass
-// is a histogram (ballot "same digit" masks, one LDS atomic per distinct digit
-// per tile) and a DPP scan that picks the digit holding the K1-th key.  It
-// stops when
+// Stage I buckets the keys by value (1024 equal-width buckets over their
+// range, one pass) and a DPP scan finds the bucket holding the K1-th smallest
+// key.  One more pass keeps every lower bucket and lists the members of that
+// boundary bucket; one thread per listed member then counts the members
+// smaller than itself in (key, index) order and keeps it if that rank is
+// below the remaining budget.  When the boundary bucket holds more than 128
+// keys (or the range is not finite), Stage I instead narrows a bucket
+// {k : (k & pmask) == prefix} that contains the K1-th key with 8-bit digit
+// passes over the highest still-undecided bits in which some key differs
+// (bytes no key varies in cost nothing): each pass is a histogram (ballot
+// "same digit" masks, one LDS atomic per distinct digit per tile) and a DPP
+// scan that picks the digit holding the K1-th key.  It stops when
 //   - the bucket holds a single key value T: keys < T are kept, then the first
 //     keys == T in token order (ordered ballot counts), or
-//   - the bucket holds at most 128 keys: each bucket member counts the members
-//     smaller than itself in (key, index) order, exactly, and is kept if that
-//     rank is below the remaining budget.
+//   - the bucket holds at most 128 keys: ranked as above.
 // Stage II buckets X^rem by value, 1024 buckets of equal width over the
-// [min, max] of its keys, in one pass; every token then counts the members of
-// its own bucket smaller in (key, index) order, so its rank in the sorted
-// X^rem is exact.  If a bucket exceeds 256 tokens or the range is not finite,
-// Stage II falls back to a stable LSD radix sort of the 16-bit indices of
-// X^rem (ordered compaction first, digits looked up by index, per-wavefront
-// scatter offsets, passes over constant bytes skipped).
+// [min, max] of its keys, in one pass; every token's rank in the sorted
+// X^rem is then its bucket's start plus the number of its bucket's members
+// smaller in (key, index) order, counted exactly: per token for small images,
+// a whole bucket per wavefront for large ones (shared by several workgroups
+// that each rank a fixed share of the buckets).  If a bucket exceeds 256
+// tokens or the range is not finite, Stage II falls back to a stable LSD radix
+// sort of the 16-bit indices of X^rem (ordered compaction first, digits looked
+// up by index, per-wavefront scatter offsets, passes over constant bytes
+// skipped).
 //
 // Every wavefront owns a contiguous, 64-aligned range of tokens for the
 // ordered steps (tie marking, compaction, output), so all results are exact
@@ -57,8 +64,10 @@ __host__ __device__ inline size_t align_up(size_t v, size_t a) { return (v + a -
 
 //   ks    u32[n]        Stage II keys by token index
 //   ki    u32[n]        Stage I keys; after Stage I the same bytes hold the
-//                       u16 bucket list of X^rem, or the two u16[n] index
-//                       buffers of the radix sort
+//                       u16 bucket list of X^rem (lower half) and each
+//                       token's u16 bucket (upper half), then the dense
+//                       ranking's per-wavefront pairs above the list; or the
+//                       two u16[n] index buffers of the radix sort
 //   bimp  u32[nw]       X^imp bitmap (nw = 2 ceil(n / 64))
 //   bsel  u32[nw]       X^imp U X^div bitmap
 //   area  u32[2048]     16-byte aligned, reused by phase:
