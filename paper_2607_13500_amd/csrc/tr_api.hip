@@ -180,6 +180,7 @@ struct tr_ctx {
     int eb = 4;
     int lds_limit = 0;
     int cap_n = 0;
+    int cus = 256;                // compute units of the device
     float* key_imp = nullptr;
     float* key_s = nullptr;
     int32_t* rows = nullptr;
@@ -216,7 +217,7 @@ hipError_t run_select(const tr_ctx* c, const Plan& pl, const float* key_imp, con
         a.nimg = B;
         a.img0 = 0;
         a.desc[0] = pl.desc[0];
-        a.groups = tr::select_groups(pl.nmax);
+        a.groups = tr::select_groups(tr::select_shares(pl.desc[0]) ? B : 0, c->cus);
         return tr::launch_select(a, pl.nmax, s);
     }
     for (int b0 = 0; b0 < B; b0 += tr::kMaxDescPerLaunch) {
@@ -224,12 +225,13 @@ hipError_t run_select(const tr_ctx* c, const Plan& pl, const float* key_imp, con
         a.uniform = 0;
         a.nimg = nb;
         a.img0 = b0;
-        int nmax = 0;
+        int nmax = 0, large = 0;
         for (int i = 0; i < nb; ++i) {
             a.desc[i] = pl.desc[(size_t)(b0 + i)];
             if (a.desc[i].n > nmax) nmax = a.desc[i].n;
+            if (tr::select_shares(a.desc[i])) ++large;
         }
-        a.groups = tr::select_groups(nmax);
+        a.groups = tr::select_groups(large, c->cus);
         hipError_t e = tr::launch_select(a, nmax, s);
         if (e != hipSuccess) return e;
     }
@@ -312,6 +314,10 @@ tr_status tr_create(const tr_params* p, tr_ctx** out)
     c->eb = elem_bytes(p->dtype);
     c->lds_limit = lds;
     c->cap_n = cap;
+    if ((e = hipDeviceGetAttribute(&c->cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) {
+        tr_destroy(c);
+        return hip_fail(e, "hipDeviceGetAttribute");
+    }
     const size_t n = (size_t)p->max_tokens;
     const size_t gw = tr::select_gsel_words(p->max_tokens, p->max_images);
     if ((e = hipMalloc(&c->key_imp, n * sizeof(float))) != hipSuccess ||

@@ -40,8 +40,13 @@ struct SelectArgs {
 
 // Words of the split-image pick bitmaps for capacity (max_tokens, max_images).
 size_t select_gsel_words(int64_t max_tokens, int max_images);
-// Workgroups per image for a launch whose largest image has nmax tokens.
-int select_groups(int nmax);
+// Whether an image's selection is shared by several workgroups when its
+// launch has more than one workgroup per image (large remainders).
+bool select_shares(const ImageDesc& d);
+// Workgroups per image for a launch with n_large such images on a device of
+// `cus` compute units: the largest power of two (at most 64) with which they
+// still fit the compute units in one round; 1 without such images.
+int select_groups(int64_t n_large, int cus);
 
 // Threads per selection workgroup for images of at most nmax tokens.
 int select_threads(int nmax);

@@ -48,11 +48,12 @@ constexpr uint32_t kCountLimit = 128;    // Stage I: count exactly inside bucket
 constexpr int kBuckets = kThreads;       // Stage II: value buckets (one per thread in the scan)
 constexpr uint32_t kBucketLimit = 256;   // Stage II: largest bucket ranked by counting
 constexpr int kDenseRem = 4096;          // Stage II: rank whole buckets per wavefront from here
-constexpr int kSplitGroups = 16;         // workgroups sharing the ranking of one large image
+constexpr int kMaxSplitGroups = 64;      // most workgroups sharing the ranking of one large image
 constexpr uint16_t kNoBucket = 0xffff;   // Stage II bucket index of a token not in X^rem
 static_assert(kCountLimit <= (uint32_t)kThreads && kCountLimit % kWave == 0,
               "one thread per listed Stage I member, in whole wavefronts");
-static_assert((kSplitGroups & (kSplitGroups - 1)) == 0, "split ownership is a mask");
+static_assert((kMaxSplitGroups & (kMaxSplitGroups - 1)) == 0 && kMaxSplitGroups * kW <= kBuckets,
+              "split ownership is a mask; every wavefront of the groups owns a bucket");
 static_assert(kDenseRem / 2 >= 2 * kWave * kW, "dense ranking's pairs fit above the X^rem list");
 
 // ---- LDS layout (same arithmetic on host and device) -----------------------
@@ -899,7 +900,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a)
     // A large image is shared by G workgroups: each repeats the deterministic
     // Stage I and bucketing in its own LDS and ranks 1/G of the buckets into
     // the image's global pick bitmap; emit_kernel then writes the output.
-    const bool split = G > 1 && K2 > 0 && N - K1 >= kDenseRem;
+    const bool split = G > 1 && K2 > 0 && N - K1 >= kDenseRem;   // as select_shares
     if (part > 0 && !split) return;
     const LdsLayout L = lds_layout(N);
     uint32_t* ks = reinterpret_cast<uint32_t*>(smem + L.ks);
@@ -1024,9 +1025,17 @@ int select_threads(int nmax)
     return kThreads;
 }
 
-int select_groups(int nmax)
+bool select_shares(const ImageDesc& d)
 {
-    return nmax >= kDenseRem ? kSplitGroups : 1;
+    return d.k2 > 0 && d.n - d.k1 >= kDenseRem;
+}
+
+int select_groups(int64_t n_large, int cus)
+{
+    if (n_large <= 0) return 1;
+    int g = 1;
+    while (g < kMaxSplitGroups && n_large * 2 * g <= (int64_t)cus) g *= 2;
+    return g;
 }
 
 size_t select_gsel_words(int64_t max_tokens, int max_images)

@@ -291,6 +291,18 @@ def test_capacity_and_max_n():
         run_and_check(w)
 
 
+def test_many_large_images_one_workgroup_each():
+    """More images with large remainders than half the compute units: the
+    launch gives each image one workgroup, which ranks all of its buckets a
+    bucket per wavefront (the workgroup count per image is picked per launch
+    from the device's compute units; the result does not depend on it)."""
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    B = cus // 2 + 1
+    say("uniform batch of", B, "x 4160 tokens, D 64, K 64 (remainder 4139)")
+    w = synth.video(device=DEV, B=B, frames=1, positions=4160, D=64, K=64)
+    run_and_check(w)
+
+
 # ------------------------------------------------------ non-finite inputs
 
 @pytest.mark.parametrize("N,dtype", [(600, torch.bfloat16), (5000, torch.bfloat16), (300, torch.float32)])
