@@ -36,6 +36,8 @@
 // Every wavefront owns a contiguous, 64-aligned range of tokens for the
 // ordered steps (tie marking, compaction, output), so all results are exact
 // and deterministic.
+#include <type_traits>
+
 #include "tr_internal.h"
 #include "tr_wave.h"
 
@@ -58,7 +60,8 @@ static_assert(kDenseRem / 2 >= 2 * kWave * kW, "dense ranking's pairs fit above 
 
 // ---- LDS layout (same arithmetic on host and device) -----------------------
 struct LdsLayout {
-    size_t ks, ki, bimp, bsel, area, slots, misc, total;
+    size_t ks, ki, bimp, bsel, area, slots, misc, comp, total;
+    bool has_comp;
 };
 
 __host__ __device__ inline size_t align_up(size_t v, size_t a) { return (v + a - 1) & ~(a - 1); }
@@ -79,6 +82,8 @@ __host__ __device__ inline size_t align_up(size_t v, size_t a) { return (v + a -
 //                                   counts / offsets of the radix sort
 //   slots u32[8][W]     per-wavefront partial values, one row per use
 //   misc  u32[16]       broadcast slots and counters
+//   comp  u64[n]        only for n < kDenseRem: X^rem as (key << 32 | index)
+//                       in bucket order, for the per-token ranking
 __host__ __device__ inline LdsLayout lds_layout(int n)
 {
     LdsLayout L;
@@ -99,8 +104,26 @@ __host__ __device__ inline LdsLayout lds_layout(int n)
     o += 4 * 8 * kW;
     L.misc = o;
     o += 4 * 16;
+    L.has_comp = n < kDenseRem;
+    L.comp = 0;
+    if (L.has_comp) {
+        o = align_up(o, 16);
+        L.comp = o;
+        o += 8 * (size_t)n;
+    }
     L.total = o;
     return L;
+}
+
+// LDS a launch needs for images of at most nmax tokens: the layout's size is
+// not monotonic in n (comp exists only below kDenseRem), so the largest over
+// n <= nmax.
+__host__ __device__ inline size_t launch_lds(int nmax)
+{
+    const size_t big = lds_layout(nmax).total;
+    if (nmax < kDenseRem) return big;
+    const size_t small = lds_layout(kDenseRem - 1).total;
+    return big > small ? big : small;
 }
 
 // ---- helpers -------------------------------------------------------------------
@@ -583,6 +606,10 @@ constexpr int kS2Global = 2;   // this group's picks are in the global bitmap
 //                 ranks
 //   pairs         2 kWave words per wavefront for the dense ranking (may
 //                 overlap dgs, which is dead by then)
+//   comp  u64[n]  or null: for the per-token ranking, X^rem as
+//                 (key << 32 | index) in bucket order, listed instead of
+//                 `list` (one LDS read per compared member instead of two
+//                 dependent ones)
 // H (B words) must be zero.  Returns kS2Failed, having written only H, cur,
 // dgs, list and slot rows, when a bucket holds more than kBucketLimit tokens
 // or the key range is not finite.
@@ -590,7 +617,7 @@ __device__ int stage2_bucket(const uint32_t* ks, const uint32_t* bimp, uint32_t*
                               int R, const Stride& sp, uint32_t* H, uint32_t* cur, uint16_t* list,
                               uint16_t* dgs, uint32_t* pairs, uint32_t* row_lo, uint32_t* row_hi,
                               uint32_t* row_a, uint32_t* row_b, int part, int parts,
-                              uint32_t* gpick, bool have_range)
+                              uint32_t* gpick, bool have_range, uint64_t* comp)
 {
     const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
     int beg, end;
@@ -676,24 +703,40 @@ __device__ int stage2_bucket(const uint32_t* ks, const uint32_t* bimp, uint32_t*
     __syncthreads();
     // Dense ranking gives bucket q to wavefront q % (parts W) across the
     // groups, so to group (q / W) % parts (parts is 1 or a power of two).
+    // The per-token ranking reads X^rem packed as (key, index) when the
+    // layout has room for it and buckets hold a member or more on average
+    // (packing costs a wider store per member; with fewer members per bucket
+    // there is little to compare: 576 tokens 0.56 -> 0.76 us of listing for
+    // no ranking gain; 2880 tokens 4.4 -> 3.3 us of ranking).
     const bool dense = R >= kDenseRem;
-    for (int base = beg; base < end; base += kTileUnr * kWave) {
-        uint32_t g[kTileUnr];
-        bool own[kTileUnr];
+    const bool pack = !dense && comp != nullptr && R >= kBuckets;
+    auto list_pass = [&](auto packed) {   // one loop per form: the choice is per image
+        for (int base = beg; base < end; base += kTileUnr * kWave) {
+            uint32_t g[kTileUnr];
+            bool own[kTileUnr];
 #pragma unroll
-        for (int u = 0; u < kTileUnr; ++u) {
-            const int i = base + u * kWave + lane;
-            g[u] = i < end ? dgs[i] : kNoBucket;
+            for (int u = 0; u < kTileUnr; ++u) {
+                const int i = base + u * kWave + lane;
+                g[u] = i < end ? dgs[i] : kNoBucket;
+            }
+#pragma unroll
+            for (int u = 0; u < kTileUnr; ++u) {   // all cursor atomics, then the stores
+                own[u] = g[u] != kNoBucket && (!dense || ((g[u] / kW) & (parts - 1)) == (uint32_t)part);
+                if (own[u]) g[u] = atomicAdd(&cur[g[u]], 1u);
+            }
+#pragma unroll
+            for (int u = 0; u < kTileUnr; ++u) {
+                const int i = base + u * kWave + lane;
+                if constexpr (decltype(packed)::value) {
+                    if (own[u]) comp[g[u]] = ((uint64_t)ks[i] << 32) | (uint32_t)i;
+                } else {
+                    if (own[u]) list[g[u]] = (uint16_t)i;
+                }
+            }
         }
-#pragma unroll
-        for (int u = 0; u < kTileUnr; ++u) {   // all cursor atomics, then the stores
-            own[u] = g[u] != kNoBucket && (!dense || ((g[u] / kW) & (parts - 1)) == (uint32_t)part);
-            if (own[u]) g[u] = atomicAdd(&cur[g[u]], 1u);
-        }
-#pragma unroll
-        for (int u = 0; u < kTileUnr; ++u)
-            if (own[u]) list[g[u]] = (uint16_t)(base + u * kWave + lane);
-    }
+    };
+    if (pack) list_pass(std::true_type{});
+    else list_pass(std::false_type{});
     __syncthreads();
     if (dense) {
         // Dense buckets: a wavefront ranks a whole bucket at a time, one
@@ -758,7 +801,23 @@ __device__ int stage2_bucket(const uint32_t* ks, const uint32_t* bimp, uint32_t*
         const int i = base + lane;
         const bool rem = i < end && !bit_of(bimp, i);
         bool picked = false;
-        if (rem) {
+        if (rem && pack) {
+            const uint32_t key = ks[i];
+            const uint64_t me = ((uint64_t)key << 32) | (uint32_t)i;
+            const int dg = value_bucket(key, fmin, scale);
+            const uint32_t stop = cur[dg];
+            uint32_t j = stop - H[dg];
+            uint32_t r = j;
+            for (; j + 8 <= stop; j += 8) {   // eight independent reads in flight
+                uint64_t c[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) c[u] = comp[j + u];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) r += c[u] < me ? 1u : 0u;
+            }
+            for (; j < stop; ++j) r += comp[j] < me ? 1u : 0u;
+            picked = sp.picks(r);
+        } else if (rem) {
             const uint32_t key = ks[i];
             const int dg = value_bucket(key, fmin, scale);
             const uint32_t stop = cur[dg];
@@ -962,7 +1021,8 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a)
         // room for 2 kWave words per wavefront once N >= kDenseRem.
         int st = stage2_bucket(ks, bimp, bsel, N, N - K1, sp, area, area + kBuckets, idx, idx + N,
                                ki + (N + 1) / 2, slots + 6 * kW, slots + 7 * kW, slots + 2 * kW,
-                               slots + 3 * kW, split ? part : 0, split ? G : 1, gpick, s2_range);
+                               slots + 3 * kW, split ? part : 0, split ? G : 1, gpick, s2_range,
+                               L.has_comp ? reinterpret_cast<uint64_t*>(smem + L.comp) : nullptr);
         if (st == kS2Failed) {
             if (part > 0) return;   // the same decision in every group: group 0 sorts
             __syncthreads();        // every thread is past the bucket attempt
@@ -1046,7 +1106,7 @@ size_t select_gsel_words(int64_t max_tokens, int max_images)
 size_t select_lds_bytes(int n, int threads)
 {
     (void)threads;
-    return lds_layout(n).total;
+    return launch_lds(n);
 }
 
 hipError_t select_prepare(int lds_limit)
@@ -1061,7 +1121,7 @@ hipError_t select_prepare(int lds_limit)
 hipError_t launch_select(const SelectArgs& a, int nmax, hipStream_t s)
 {
     if (a.nimg <= 0) return hipSuccess;
-    const size_t lds = lds_layout(nmax).total;
+    const size_t lds = launch_lds(nmax);
     const int groups = a.groups > 0 ? a.groups : 1;
     hipLaunchKernelGGL(select_kernel, dim3(a.nimg * groups), dim3(kThreads), lds, s, a);
     if (groups > 1) {
