@@ -162,7 +162,7 @@ def test_misaligned_pointers_give_identical_results():
     r.close()
 
 
-def _select_cases(rng, trials=60):
+def _select_cases(rng, trials=200):
     cases = []
     for trial in range(trials):
         B = int(rng.integers(1, 7))

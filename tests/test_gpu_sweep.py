@@ -4,6 +4,7 @@ tr_reduce, each checked against the fp64 oracle with the parity protocol
 widths that are and are not multiples of the vector width, bf16 and fp32,
 lambda in [0, 1], K from 1 to N, both stride readings and both entropies,
 with exact duplicate rows and all-zero rows sprinkled in."""
+import os
 import random
 import sys
 
@@ -45,12 +46,18 @@ def case(c, seed):
     return w, dtype, stride_mode, entropy
 
 
-@pytest.mark.parametrize("c", range(60))
-def test_random_case_matches_oracle(c):
+# TR_SWEEP_CASES cases per seed of TR_SWEEP_SEEDS (comma-separated); the
+# defaults take a few seconds on one MI355X.
+CASES = int(os.environ.get("TR_SWEEP_CASES", "300"))
+SEEDS = [int(x) for x in os.environ.get("TR_SWEEP_SEEDS", "1").split(",") if x.strip()]
+
+
+@pytest.mark.parametrize("seed,c", [(s, c) for s in SEEDS for c in range(CASES)])
+def test_random_case_matches_oracle(seed, c):
     import paper_2607_13500_amd as tr
-    w, dtype, stride_mode, entropy = case(c, seed=1)
-    print("[case] sweep %d: B=%d N=%s D=%d Dc=%d %s lam=%.3f K=%s stride=%d entropy=%d"
-          % (c, len(w.N), w.N, w.D, w.Dc, str(dtype).split(".")[-1], w.lam, w.K, stride_mode, entropy),
+    w, dtype, stride_mode, entropy = case(c, seed=seed)
+    print("[case] sweep seed %d case %d: B=%d N=%s D=%d Dc=%d %s lam=%.3f K=%s stride=%d entropy=%d"
+          % (seed, c, len(w.N), w.N, w.D, w.Dc, str(dtype).split(".")[-1], w.lam, w.K, stride_mode, entropy),
           flush=True)
     sys.stdout.flush()
     r = tr.Reducer(w.D, w.Dc, dtype, lam=w.lam, max_images=len(w.N), max_tokens=sum(w.N),
