@@ -919,32 +919,45 @@ __device__ void stage2_radix(const uint32_t* ks, const uint32_t* bimp, uint32_t*
     }
 }
 
+// Lane t's value of a 64-bit register, on every lane (t wavefront-uniform).
+__device__ __forceinline__ uint64_t lane_u64(uint64_t v, int t)
+{
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, t);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), t);
+    return ((uint64_t)hi << 32) | lo;
+}
+
 // X* in ascending token index: out_idx (image-local), out_src, out_rows.
+// Lane t of each wavefront holds the 64-bit bsel and bimp words of the
+// wavefront's t-th tile (a range has at most 64 tiles at the capacity's N),
+// so the counts and the ordered writes read LDS once per wavefront.
 __device__ void emit(const SelectArgs& a, const Img& d, const uint32_t* bimp, const uint32_t* bsel,
                      uint32_t* row)
 {
     const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
     int beg, end;
     wave_range(d.n, w, beg, end);
-    uint32_t oc = 0;
-    for (int base = beg; base < end; base += kWave) {
-        const int i = base + lane;
-        oc += __popcll(__ballot(i < end && bit_of(bsel, i)));
+    const int tiles = (end - beg + kWave - 1) / kWave;
+    uint64_t sel = 0, imp = 0;
+    if (lane < tiles) {
+        sel = *reinterpret_cast<const uint64_t*>(bsel + ((beg >> 5) + 2 * lane));
+        imp = *reinterpret_cast<const uint64_t*>(bimp + ((beg >> 5) + 2 * lane));
+        const int valid = end - (beg + kWave * lane);   // tokens of this tile inside the image
+        if (valid < kWave) sel &= (1ull << valid) - 1ull;
     }
-    uint32_t opos = wave_prefix(oc, row);
+    uint32_t opos = wave_prefix(wave_sum_u32((uint32_t)__popcll(sel)), row);
     const int K = d.k1 + d.k2;
-    for (int base = beg; base < end; base += kWave) {
-        const int i = base + lane;
-        const bool kept = i < end && bit_of(bsel, i);
-        const uint64_t bk = __ballot(kept);
-        const int slot = (int)opos + __popcll(bk & lanes_below(lane));
-        if (kept && slot < K) {   // never more than K writes, whatever the keys
+    for (int t = 0; t < tiles; ++t) {
+        const uint64_t m = lane_u64(sel, t), im = lane_u64(imp, t);
+        const int i = beg + kWave * t + lane;
+        const int slot = (int)opos + __popcll(m & lanes_below(lane));
+        if (((m >> lane) & 1ull) && slot < K) {   // never more than K writes, whatever the keys
             const int o = d.out_off + slot;
             a.out_idx[o] = i;
-            if (a.out_src) a.out_src[o] = bit_of(bimp, i) ? 0 : 1;
+            if (a.out_src) a.out_src[o] = ((im >> lane) & 1ull) ? 0 : 1;
             if (a.out_rows) a.out_rows[o] = d.row_off + i;
         }
-        opos += (uint32_t)__popcll(bk);
+        opos += (uint32_t)__popcll(m);
     }
 }
 
