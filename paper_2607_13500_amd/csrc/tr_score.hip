@@ -36,7 +36,9 @@
 // Every u is formed as 1 + e with e = (|x| - c) (1/c) + delta, delta =
 // c (1/c) - 1 taken exactly by a fused multiply-add, so all terms (and r)
 // refer to the same effective shift 1 / (1/c) and e keeps full relative
-// accuracy for near-uniform rows.  A row whose probe mean is 0 uses the plain
+// accuracy for near-uniform rows.  The terms are summed in base-2 units
+// (e / ln 2 and g / ln 2), which saves a multiply per element; the row's sum
+// is scaled by ln 2 once.  A row whose probe mean is 0 uses the plain
 // form H1 = log S - (sum |x| log |x|) / S instead.
 #include "tr_score.h"
 #include "tr_wave.h"
@@ -132,39 +134,44 @@ __device__ __forceinline__ void x_chunk(XAcc& a, const float* v, int m, float c)
     }
 }
 
-// g(1 + e) = (1 + e) log(1 + e) - e >= 0, given e (and u = 1 + e for the
-// direct form).  For |e| < 1/4 as e^2 phi(e), phi a degree-5 polynomial (the
-// Chebyshev interpolant of g(1 + e) / e^2 on [-1/4, 1/4], relative error
+// Base-2 units: y = e / ln 2 and g2(y) = g(1 + e) / ln 2 >= 0, given y (and
+// u = 1 + e for the direct form); the row's sum is multiplied by ln 2 once.
+// For |e| < 1/4 as y^2 psi(y), psi a degree-5 polynomial (the Chebyshev
+// interpolant of g(1 + e) / (y^2 ln 2) on |y| < (1/4) / ln 2, relative error
 // 3e-7, 4e-7 with fp32 Horner; coefficients from gen_shannon_poly.py), which
 // keeps full relative accuracy where the direct form cancels (in fp32 the
 // direct form's error grows to 1e-5 at |e| = 1/8, so the cut stays at 1/4);
-// elsewhere u log u - e with the
-// hardware base-2 logarithm (argument clamped to 1e-30, a normal number, so
-// u = 0 gives 0 - e = 1).  Both forms are evaluated and one is selected: no
-// per-element divergence.
-__device__ __forceinline__ float g_shannon(float e, float u)
+// elsewhere u log2 u - y with the hardware base-2 logarithm (argument clamped
+// to 1e-30, a normal number, so u = 0 gives 0 - y = 1 / ln 2).  Both forms
+// are evaluated and one is selected: no per-element divergence.
+constexpr float kInvLn2 = 1.44269504088896340736f;
+constexpr float kLn2 = 0.693147180559945309f;
+constexpr float kShannonCut = 0.25f * kInvLn2;   // |e| < 1/4 in units of y
+
+__device__ __forceinline__ float g2_shannon(float y, float u)
 {
-    float p = -2.541277015e-02f;
-    p = fmaf(p, e, 3.508703353e-02f);
-    p = fmaf(p, e, -4.994899918e-02f);
-    p = fmaf(p, e, 8.329159454e-02f);
-    p = fmaf(p, e, -1.666670687e-01f);
-    p = fmaf(p, e, 5.000001460e-01f);
-    const float series = (e * e) * p;
-    constexpr float kLn2 = 0.693147180559945309f;
-    const float direct = fmaf(u * kLn2, __builtin_amdgcn_logf(fmaxf(u, 1e-30f)), -e);
-    return fabsf(e) < 0.25f ? series : direct;
+    float p = -2.818413918e-03f;
+    p = fmaf(p, y, 5.614020020e-03f);
+    p = fmaf(p, y, -1.152998215e-02f);
+    p = fmaf(p, y, 2.773815429e-02f);
+    p = fmaf(p, y, -8.007569547e-02f);
+    p = fmaf(p, y, 3.465736915e-01f);
+    const float series = (y * y) * p;
+    const float direct = fmaf(u, __builtin_amdgcn_logf(fmaxf(u, 1e-30f)), -y);
+    return fabsf(y) < kShannonCut ? series : direct;
 }
 
-// Shannon partial sums over m elements for a row shift c > 0 (inv = 1/c,
-// delta = c inv - 1): sd as for CV^2, sd2 = sum g(|x| / c).
+// Shannon partial sums over m elements for a row shift c > 0 (inv = 1/c;
+// inv2 = inv / ln 2 and delta2 = (c inv - 1) / ln 2 give y): sd as for CV^2,
+// sd2 = sum g(|x| / c) / ln 2.
 __device__ __forceinline__ void x_chunk_shannon(XAcc& a, const float* v, int m, float c, float inv,
-                                                float delta)
+                                                float inv2, float delta2)
 {
     for (int k = 0; k < m; ++k) {
         const float ax = fabsf(v[k]);
-        a.sd += ax - c;
-        a.sd2 += g_shannon(fmaf(ax - c, inv, delta), ax * inv);
+        const float d = ax - c;
+        a.sd += d;
+        a.sd2 += g2_shannon(fmaf(d, inv2, delta2), ax * inv);
     }
 }
 
@@ -174,7 +181,7 @@ __device__ __forceinline__ void x_chunk_shannon_plain(XAcc& a, const float* v, i
     for (int k = 0; k < m; ++k) {
         const float ax = fabsf(v[k]);
         a.sd += ax;
-        a.sd2 = fmaf(ax * 0.693147180559945309f, __builtin_amdgcn_logf(fmaxf(ax, 1e-30f)), a.sd2);
+        a.sd2 = fmaf(ax * kLn2, __builtin_amdgcn_logf(fmaxf(ax, 1e-30f)), a.sd2);
     }
 }
 
@@ -266,18 +273,20 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a)
 
     XAcc xa{0.f, 0.f};
     CAcc ca{0.f, 0.f, 0.f};
-    float c = 0.f, inv_c = 0.f, delta = 0.f;
+    float c = 0.f, inv_c = 0.f, delta = 0.f, inv2 = 0.f, delta2 = 0.f;
     // 1/c and its exact rounding offset for the Shannon terms.
     auto set_shift = [&](float cc) {
         c = cc;
         if constexpr (kH1) {
             inv_c = c > 0.f ? 1.f / c : 0.f;
             delta = c > 0.f ? fmaf(c, inv_c, -1.f) : 0.f;
+            inv2 = inv_c * kInvLn2;
+            delta2 = delta * kInvLn2;
         }
     };
     auto x_acc = [&](const float* v, int m) {
         if constexpr (kH1) {
-            if (c > 0.f) x_chunk_shannon(xa, v, m, c, inv_c, delta);   // c is wave-uniform
+            if (c > 0.f) x_chunk_shannon(xa, v, m, c, inv_c, inv2, delta2);   // c is wave-uniform
             else x_chunk_shannon_plain(xa, v, m);
         } else {
             x_chunk(xa, v, m, c);
@@ -347,7 +356,7 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a)
             } else if (c > 0.f) {
                 const float rm1 = fmaf(sd / Df, inv_c, delta);   // r - 1
                 const float r = 1.f + rm1;
-                const float dkl = (sd2 - Df * g_shannon(rm1, r)) / r;
+                const float dkl = kLn2 * (sd2 - Df * g2_shannon(rm1 * kInvLn2, r)) / r;
                 cv2 = fmaxf(0.f, dkl / Df);
                 h2 = a.logD - cv2;
             } else {   // probe mean 0: sd = sum |x|, sd2 = sum |x| log |x|
