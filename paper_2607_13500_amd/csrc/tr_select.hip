@@ -431,7 +431,8 @@ __device__ void stage1_narrow(const uint32_t* ki, int N, uint32_t VI, uint32_t* 
 }
 
 // Value bucket of a key: floor((v - fmin) * scale) clamped to the last
-// bucket, non-decreasing in the key.
+// bucket, non-decreasing in the key.  Callers guarantee a finite width and
+// scale, so for keys in [fmin, fmax] the product is finite and in range.
 __device__ __forceinline__ int value_bucket(uint32_t key, float fmin, float scale)
 {
     return min(kBuckets - 1, (int)((key_value(key) - fmin) * scale));
@@ -458,6 +459,7 @@ __device__ bool stage1_bucket(const uint32_t* ki, const uint32_t* ks, int N, uin
     const float width = key_value(kimax) - fmin;
     if (!(width > 0.f) || !(width < 3.0e38f)) return false;
     const float scale = (float)kBuckets / width;
+    if (!(scale < 3.0e38f)) return false;   // a range of denormals: bucket arithmetic would overflow
     for (int base = beg; base < end; base += kTileUnr * kWave) {
         uint32_t k[kTileUnr];
         load_tiles(ki, base, end, lane, k);
@@ -673,6 +675,7 @@ __device__ int stage2_bucket(const uint32_t* ks, const uint32_t* bimp, uint32_t*
     const float width = key_value(kmax) - fmin;
     if (!(width > 0.f) || !(width < 3.0e38f)) return kS2Failed;   // not finite: sort instead
     const float scale = (float)kBuckets / width;
+    if (!(scale < 3.0e38f)) return kS2Failed;   // a range of denormals: sort instead
 
     for (int base = beg; base < end; base += kTileUnr * kWave) {
         uint32_t k[kTileUnr];

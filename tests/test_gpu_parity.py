@@ -184,7 +184,7 @@ def _select_cases(rng, trials=200):
     # one outlier that puts every other key in one bucket, narrow clusters
     shaped = []
     for n in (100, 576, 3000, 4096, 5000):
-        for shape in ("const", "outlier", "narrow"):
+        for shape in ("const", "outlier", "narrow", "denormal"):
             shaped.append(([n], [max(1, n // 9)], 1 / 3, shape))
     return [c + ("mixed",) for c in cases] + shaped
 
@@ -204,6 +204,12 @@ def _select_keys(rng, shape, total):
         ki[total // 2] = 4095.0
         ks = (0.3 + 1e-3 * rng.standard_normal(total)).astype(np.float32)
         ks[total // 3] = -1.0
+    elif shape == "denormal":
+        # subnormal keys (and zeros) of both signs: a key range too narrow for
+        # the value buckets' arithmetic, so the integer fallbacks decide
+        ki = rng.integers(0, 3000, total).astype(np.uint32).view(np.float32).copy()
+        ks = rng.integers(0, 500, total).astype(np.uint32).view(np.float32).copy()
+        ks = np.where(rng.random(total) < 0.5, -ks, ks).astype(np.float32)
     else:
         ki = (1.0 + 1e-6 * rng.integers(0, 40, total)).astype(np.float32)
         ks = (0.5 + 1e-7 * rng.integers(0, 300, total)).astype(np.float32)
