@@ -180,6 +180,10 @@ def _select_cases(rng, trials=200):
     cases.append(([4096], [512], 0.0))
     cases.append(([4097, 4099, 4096], [3, 700, 4096], 0.0))
     cases.append(([4098], [6], 1 / 3))
+    # a launch whose largest image (4096 tokens) has no packed-remainder
+    # region while a smaller one (4095) has it: the launch must reserve the
+    # larger layout of the smaller image
+    cases.append(([4096, 4095, 2048, 1100], [400, 409, 256, 120], 1 / 3))
     # key shapes that steer the selection's internal paths: all keys equal,
     # one outlier that puts every other key in one bucket, narrow clusters
     shaped = []
