@@ -45,6 +45,12 @@
  * Errors: argument and capacity errors return TR_EINVAL (or TR_EUNSUPPORTED)
  * synchronously with nothing enqueued.  TR_EDEVICE reports a HIP failure at
  * launch.  tr_last_error gives a one-line description of the latest failure.
+ *
+ * Alignment: every tensor base must be aligned to its element size (2 bytes
+ * for bf16, 4 for fp32 and for the int32 / float outputs); a base that is not
+ * is an unsupported alignment, TR_EUNSUPPORTED.  Beyond that, 16-byte aligned
+ * bases and row pitches take the vector path and others a scalar path with
+ * bit-identical results.
  */
 #ifndef TR_H
 #define TR_H
@@ -109,7 +115,9 @@ typedef struct {
  * fits the per-image selection's on-chip memory.  Returns TR_EINVAL for a bad
  * field, TR_EUNSUPPORTED when max_N exceeds the selection capacity
  * (tr_capacity_N), TR_ENOMEM or TR_EDEVICE on runtime failure.  *out is NULL
- * on failure. */
+ * on failure and nothing stays allocated.  Test hook: the environment
+ * variable TR_FAIL_ALLOC = k (k >= 1) makes the k-th device allocation of
+ * each tr_create call fail as if the device were out of memory. */
 tr_status tr_create(const tr_params* p, tr_ctx** out);
 
 /* The whole module (steps 1-7 above) on a packed batch of B images.
@@ -127,9 +135,8 @@ tr_status tr_create(const tr_params* p, tr_ctx** out);
  *          TR_FLAG_SHANNON)
  *   out_s  device float [sum N] or NULL: s of every token
  *   stream hipStream_t or NULL
- * X, X_pre, X_post and out may have any alignment (16-byte aligned bases and
- * row pitches take the vector path; others a scalar path with bit-identical
- * results).
+ * Bases not aligned to their element size give TR_EUNSUPPORTED (see
+ * Alignment above).
  * A score that decides nothing is not computed and its inputs are not read:
  * H2 when every image has K1 = 0 or K1 = N (lambda = 0, the paper's ablation
  * without the importance stage) and out_h2 is NULL; s when every image has
@@ -230,6 +237,17 @@ tr_status tr_reduce_project(tr_ctx* ctx, const void* X, const void* X_pre,
                             const int32_t* K, const void* W, int64_t ldw,
                             int32_t Nout, void* out, int32_t* out_idx,
                             uint8_t* out_src, void* stream);
+
+/* Host-only check of a tr_reduce call (Algorithm 1's REQUIRE: 1 <= K_b <=
+ * N_b, lambda in [0, 1]; and the argument rules above): the status tr_reduce
+ * would return for these arguments, without a device or a context.  p's
+ * capacity fields apply where they are > 0; the device's selection capacity
+ * (tr_capacity_N) is not checked.  Pointers are only inspected, never
+ * dereferenced. */
+tr_status tr_check_reduce(const tr_params* p, const void* X, const void* X_pre, const void* X_post,
+                          int32_t B, const int32_t* N, const int32_t* K, const void* out,
+                          const int32_t* out_idx, const uint8_t* out_src, const float* out_h2,
+                          const float* out_s);
 
 /* Host-only budget plan (Algorithm 1, step 1 and the stride of step 6) with
  * the same validation tr_reduce applies; needs no device.  p may carry zero

@@ -99,6 +99,10 @@ class ReduceResult(NamedTuple):
     s: Optional[torch.Tensor]      # [sum N] float32
 
 
+def _flags(stride_real: bool, shannon: bool) -> int:
+    return (_lib.TR_FLAG_STRIDE_REAL if stride_real else 0) | (_lib.TR_FLAG_SHANNON if shannon else 0)
+
+
 class Reducer:
     """A library context bound to one device, row widths, dtype and lambda.
 
@@ -123,7 +127,7 @@ class Reducer:
             max_N = min(capacity_N_on(self.device), int(max_tokens))
         self.max_images, self.max_tokens, self.max_N = int(max_images), int(max_tokens), int(max_N)
         self.stride_real, self.shannon = bool(stride_real), bool(shannon)
-        flags = (_lib.TR_FLAG_STRIDE_REAL if stride_real else 0) | (_lib.TR_FLAG_SHANNON if shannon else 0)
+        flags = _flags(stride_real, shannon)
         p = _params(D, Dc, dtype, lam, keep_ratio, max_images, max_tokens, max_N, flags)
         ctx = ctypes.c_void_p()
         with torch.cuda.device(self.device):

@@ -69,6 +69,8 @@ def load(build_if_missing: bool = True) -> ctypes.CDLL:
     lib.tr_reduce_project.restype = i32
     lib.tr_read_bandwidth.argtypes = [vp, vp, i32, vp, i32, vp]
     lib.tr_read_bandwidth.restype = i32
+    lib.tr_check_reduce.argtypes = [P(Params), vp, vp, vp, i32, vp, vp, vp, vp, vp, vp, vp]
+    lib.tr_check_reduce.restype = i32
     lib.tr_plan.argtypes = [P(Params), i32, vp, vp, vp, vp, vp, vp]
     lib.tr_plan.restype = i32
     lib.tr_capacity_N.argtypes = []

@@ -15,7 +15,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libaltr.so")
-SOURCES = ["tr_api.hip", "tr_score.hip", "tr_select.hip", "tr_gather.hip", "tr_gemm.hip", "tr_measure.hip"]
+SOURCES = ["tr_plan.cpp", "tr_api.hip", "tr_score.hip", "tr_select.hip", "tr_gather.hip", "tr_gemm.hip", "tr_measure.hip"]
 ARCH = "gfx950"
 
 

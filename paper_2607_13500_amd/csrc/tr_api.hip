@@ -3,31 +3,25 @@
 #include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <new>
-#include <string>
 #include <vector>
 
 #include "tr.h"
 #include "tr_internal.h"
 
+using tr::CallPtrs;
+using tr::check_params;
+using tr::clear_error;
+using tr::elem_bytes;
+using tr::fail;
 using tr::ImageDesc;
+using tr::make_plan;
+using tr::Plan;
 
 namespace {
-
-thread_local std::string g_err;
-
-tr_status fail(tr_status st, const char* fmt, ...)
-{
-    char buf[512];
-    va_list ap;
-    va_start(ap, fmt);
-    vsnprintf(buf, sizeof buf, fmt, ap);
-    va_end(ap);
-    g_err = buf;
-    return st;
-}
 
 tr_status hip_fail(hipError_t e, const char* what)
 {
@@ -36,104 +30,6 @@ tr_status hip_fail(hipError_t e, const char* what)
 
 constexpr int kTimedCalls = 1024;
 constexpr int kLdsFallback = 65536;
-
-int elem_bytes(int32_t dtype) { return dtype == TR_BF16 ? 2 : 4; }
-
-// Checks of the problem statement shared by tr_create and tr_plan.
-tr_status check_params(const tr_params* p, bool need_caps)
-{
-    if (!p) return fail(TR_EINVAL, "params is NULL");
-    if (p->D <= 0) return fail(TR_EINVAL, "D must be > 0 (got %d)", p->D);
-    if (p->Dc < 0) return fail(TR_EINVAL, "Dc must be >= 0 (got %d)", p->Dc);
-    if (p->dtype != TR_FP32 && p->dtype != TR_BF16)
-        return fail(TR_EINVAL, "dtype must be TR_FP32 or TR_BF16 (got %d)", p->dtype);
-    if (p->flags & ~(int32_t)(TR_FLAG_STRIDE_REAL | TR_FLAG_SHANNON))
-        return fail(TR_EINVAL, "unknown flags 0x%x", p->flags);
-    if (!(p->lambda >= 0.0 && p->lambda <= 1.0))
-        return fail(TR_EINVAL, "lambda must be in [0, 1] (got %g)", p->lambda);
-    if (!(p->keep_ratio == 0.0 || (p->keep_ratio > 0.0 && p->keep_ratio <= 1.0)))
-        return fail(TR_EINVAL, "keep_ratio must be 0 (unused) or in (0, 1] (got %g)", p->keep_ratio);
-    const int64_t eb = elem_bytes(p->dtype);
-    const int64_t dc = p->Dc ? p->Dc : p->D;
-    if ((int64_t)p->D * eb > (int64_t)INT32_MAX || dc * eb > (int64_t)INT32_MAX)
-        return fail(TR_EINVAL, "row too wide");
-    if (need_caps) {
-        if (p->max_images < 1) return fail(TR_EINVAL, "max_images must be >= 1");
-        if (p->max_tokens < 1 || p->max_tokens > (int64_t)INT32_MAX)
-            return fail(TR_EINVAL, "max_tokens must be in [1, 2^31 - 1]");
-        if (p->max_N < 1) return fail(TR_EINVAL, "max_N must be >= 1");
-    }
-    return TR_OK;
-}
-
-struct Plan {
-    std::vector<ImageDesc> desc;
-    int64_t sum_n = 0;
-    int64_t sum_k = 0;
-    int nmax = 0;
-    bool uniform = true;
-    bool keys_imp = false;   // some image's Stage I depends on the key order (0 < K1 < N)
-    bool keys_s = false;     // some image's Stage II does (0 < K2 < N - K1)
-};
-
-// Algorithm 1, step 1 (K1 = floor(lambda K) in double, K2 = K - K1) and the
-// stride t = max(1, floor((N - K1) / K2)), with every per-image check.
-tr_status make_plan(const tr_params* p, int32_t B, const int32_t* N, const int32_t* K, Plan& out)
-{
-    if (B < 0) return fail(TR_EINVAL, "B must be >= 0 (got %d)", B);
-    if (p->max_images > 0 && B > p->max_images)
-        return fail(TR_EINVAL, "B = %d exceeds max_images = %d", B, p->max_images);
-    if (B > 0 && !N) return fail(TR_EINVAL, "N is NULL");
-    if (B > 0 && !K && !(p->keep_ratio > 0.0))
-        return fail(TR_EINVAL, "K is NULL and no keep_ratio was set");
-    out.desc.resize((size_t)B);
-    int64_t rows = 0, outs = 0;
-    for (int32_t b = 0; b < B; ++b) {
-        const int32_t n = N[b];
-        if (n < 1) return fail(TR_EINVAL, "N[%d] = %d must be >= 1", b, n);
-        if (n > 65535) return fail(TR_EINVAL, "N[%d] = %d exceeds 65535", b, n);
-        if (p->max_N > 0 && n > p->max_N)
-            return fail(TR_EINVAL, "N[%d] = %d exceeds max_N = %d", b, n, p->max_N);
-        int32_t k;
-        if (K) {
-            k = K[b];
-        } else {
-            const double kr = floor(p->keep_ratio * (double)n);
-            k = kr < 1.0 ? 1 : (kr > (double)n ? n : (int32_t)kr);
-        }
-        if (k < 1 || k > n) return fail(TR_EINVAL, "K[%d] = %d must be in [1, N = %d]", b, k, n);
-        const int32_t k1 = (int32_t)floor(p->lambda * (double)k);
-        const int32_t k2 = k - k1;
-        int32_t t = 0;
-        if (k2 > 0) {
-            t = (n - k1) / k2;
-            if (t < 1) t = 1;
-        }
-        ImageDesc& d = out.desc[(size_t)b];
-        d.row_off = (int32_t)rows;
-        d.n = n;
-        d.k1 = k1;
-        d.k2 = k2;
-        d.t = t;
-        d.out_off = (int32_t)outs;
-        if (k1 > 0 && k1 < n) out.keys_imp = true;
-        if (k2 > 0 && k2 < n - k1) out.keys_s = true;
-        rows += n;
-        outs += k;
-        if (rows > (int64_t)INT32_MAX) return fail(TR_EINVAL, "sum of N exceeds 2^31 - 1");
-        if (n > out.nmax) out.nmax = n;
-        if (b > 0) {
-            const ImageDesc& d0 = out.desc[0];
-            if (d.n != d0.n || d.k1 != d0.k1 || d.k2 != d0.k2) out.uniform = false;
-        }
-    }
-    if (p->max_tokens > 0 && rows > p->max_tokens)
-        return fail(TR_EINVAL, "sum of N = %lld exceeds max_tokens = %lld", (long long)rows,
-                    (long long)p->max_tokens);
-    out.sum_n = rows;
-    out.sum_k = outs;
-    return TR_OK;
-}
 
 int lds_limit_of(int dev)
 {
@@ -155,6 +51,29 @@ int capacity_for(int lds_limit)
 }
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+// The device allocations of one tr_create call.  Test hook: with the
+// environment variable TR_FAIL_ALLOC = k (k >= 1), the k-th allocation fails
+// as if the device were out of memory (nothing is allocated for it), so that
+// the clean-up path of tr_create can be exercised on a real device.
+struct CtxAlloc {
+    int count = 0;
+    int fail_at = 0;
+    CtxAlloc()
+    {
+        const char* v = getenv("TR_FAIL_ALLOC");
+        if (v) fail_at = atoi(v);
+    }
+    template <typename T>
+    hipError_t operator()(T** ptr, size_t bytes)
+    {
+        if (++count == fail_at) {
+            *ptr = nullptr;
+            return hipErrorOutOfMemory;
+        }
+        return hipMalloc(reinterpret_cast<void**>(ptr), bytes);
+    }
+};
 
 struct DeviceGuard {
     int prev = -1;
@@ -251,20 +170,6 @@ tr_status check_ctx_plan(tr_ctx* c, int32_t B, const int32_t* N, const int32_t* 
 
 extern "C" {
 
-const char* tr_strerror(tr_status s)
-{
-    switch (s) {
-    case TR_OK: return "success";
-    case TR_EINVAL: return "invalid argument";
-    case TR_ENOMEM: return "out of memory";
-    case TR_EUNSUPPORTED: return "unsupported request";
-    case TR_EDEVICE: return "HIP device error";
-    }
-    return "unknown status";
-}
-
-const char* tr_last_error(void) { return g_err.c_str(); }
-
 int32_t tr_capacity_N(void)
 {
     int dev = 0;
@@ -272,28 +177,9 @@ int32_t tr_capacity_N(void)
     return capacity_for(lds_limit_of(dev));
 }
 
-tr_status tr_plan(const tr_params* p, int32_t B, const int32_t* N, const int32_t* K, int32_t* Kout,
-                  int32_t* K1out, int32_t* K2out, int32_t* tout)
-{
-    g_err.clear();
-    tr_status st = check_params(p, false);
-    if (st != TR_OK) return st;
-    Plan pl;
-    st = make_plan(p, B, N, K, pl);
-    if (st != TR_OK) return st;
-    for (int32_t b = 0; b < B; ++b) {
-        const ImageDesc& d = pl.desc[(size_t)b];
-        if (Kout) Kout[b] = d.k1 + d.k2;
-        if (K1out) K1out[b] = d.k1;
-        if (K2out) K2out[b] = d.k2;
-        if (tout) tout[b] = d.t;
-    }
-    return TR_OK;
-}
-
 tr_status tr_create(const tr_params* p, tr_ctx** out)
 {
-    g_err.clear();
+    clear_error();
     if (!out) return fail(TR_EINVAL, "out is NULL");
     *out = nullptr;
     tr_status st = check_params(p, true);
@@ -320,11 +206,12 @@ tr_status tr_create(const tr_params* p, tr_ctx** out)
     }
     const size_t n = (size_t)p->max_tokens;
     const size_t gw = tr::select_gsel_words(p->max_tokens, p->max_images);
-    if ((e = hipMalloc(&c->key_imp, n * sizeof(float))) != hipSuccess ||
-        (e = hipMalloc(&c->key_s, n * sizeof(float))) != hipSuccess ||
-        (e = hipMalloc(&c->rows, n * sizeof(int32_t))) != hipSuccess ||
-        (e = hipMalloc(&c->gsel, gw * sizeof(uint32_t))) != hipSuccess ||
-        (e = hipMalloc(&c->gimp, gw * sizeof(uint32_t))) != hipSuccess) {
+    CtxAlloc al;
+    if ((e = al(&c->key_imp, n * sizeof(float))) != hipSuccess ||
+        (e = al(&c->key_s, n * sizeof(float))) != hipSuccess ||
+        (e = al(&c->rows, n * sizeof(int32_t))) != hipSuccess ||
+        (e = al(&c->gsel, gw * sizeof(uint32_t))) != hipSuccess ||
+        (e = al(&c->gimp, gw * sizeof(uint32_t))) != hipSuccess) {
         tr_destroy(c);
         return fail(TR_ENOMEM, "hipMalloc of %zu-token scratch failed: %s", n, hipGetErrorString(e));
     }
@@ -344,7 +231,7 @@ tr_status tr_create(const tr_params* p, tr_ctx** out)
     }
     if (p->dtype == TR_BF16 && c->Dc % 128 == 0) {
         const size_t words = n * (size_t)tr::gemm_part_cols(c->Dc) * 3;
-        if ((e = hipMalloc(&c->cos_part, words * sizeof(float))) != hipSuccess) {
+        if ((e = al(&c->cos_part, words * sizeof(float))) != hipSuccess) {
             tr_destroy(c);
             return fail(TR_ENOMEM, "hipMalloc of %zu cosine partials failed", words);
         }
@@ -369,7 +256,7 @@ void tr_destroy(tr_ctx* c)
 
 tr_status tr_timing_enable(tr_ctx* c, int32_t enable)
 {
-    g_err.clear();
+    clear_error();
     if (!c) return fail(TR_EINVAL, "ctx is NULL");
     DeviceGuard g(c->device);
     if (enable && c->events.empty()) {
@@ -387,7 +274,7 @@ tr_status tr_timing_enable(tr_ctx* c, int32_t enable)
 
 tr_status tr_timing_read(tr_ctx* c, double* ms, int64_t* calls)
 {
-    g_err.clear();
+    clear_error();
     if (!c || !ms) return fail(TR_EINVAL, "ctx or ms is NULL");
     DeviceGuard g(c->device);
     double acc[3] = {0, 0, 0};
@@ -443,23 +330,26 @@ tr_status reduce_impl(tr_ctx* c, ReduceCall r)
     tr_status st = check_ctx_plan(c, r.B, r.N, r.K, pl);
     if (st != TR_OK) return st;
     if (r.B == 0) return TR_OK;
-    if (!r.X || !r.out || !r.out_idx) return fail(TR_EINVAL, "X, out and out_idx must be non-NULL");
-    // Which scores the call needs: Stage I's when some image ranks by it or
-    // H2 is asked for, Stage II's likewise (lambda = 1 never needs s, lambda
-    // = 0 never needs H2).  A score that is not needed is not computed and its
-    // inputs are not read.  A supplied Stage II key replaces the s score.
-    int mode = (pl.keys_imp || r.out_h2 ? tr::kScoreImp : 0) |
-               (!r.key_s && (pl.keys_s || r.out_s) ? tr::kScoreSim : 0);
-    if ((mode & tr::kScoreImp) && (c->p.flags & TR_FLAG_SHANNON)) mode |= tr::kScoreShannon;
-    const bool need_c = (mode & tr::kScoreSim) != 0;
-    if (need_c && (!r.X_pre || !r.X_post))
-        return fail(TR_EINVAL, "X_pre and X_post must be non-NULL when Stage II ranks tokens or out_s is set");
-    if (!need_c) r.X_pre = r.X_post = nullptr;
-    const uintptr_t em = (uintptr_t)c->eb - 1;
-    if (((uintptr_t)r.X | (uintptr_t)r.X_pre | (uintptr_t)r.X_post | (uintptr_t)r.out) & em)
-        return fail(TR_EINVAL, "tensor base pointers must be aligned to the element size");
-    if (((uintptr_t)r.out_idx | (uintptr_t)r.out_h2 | (uintptr_t)r.out_s | (uintptr_t)r.key_s) & 3u)
-        return fail(TR_EINVAL, "out_idx, out_h2, out_s and key_s must be 4-byte aligned");
+    // Pointer rules, and which scores the call needs (lambda = 1 never needs
+    // s, lambda = 0 never needs H2; a supplied Stage II key replaces s).  A
+    // score that is not needed is not computed and its inputs are not read.
+    CallPtrs cp;
+    cp.X = r.X;
+    cp.X_pre = r.X_pre;
+    cp.X_post = r.X_post;
+    cp.key_s = r.key_s;
+    cp.out = r.out;
+    cp.out_idx = r.out_idx;
+    cp.out_src = r.out_src;
+    cp.out_h2 = r.out_h2;
+    cp.out_s = r.out_s;
+    bool need_x = false, need_c = false;
+    st = tr::check_call(&c->p, pl, cp, need_x, need_c);
+    if (st != TR_OK) return st;
+    r.X_pre = cp.X_pre;
+    r.X_post = cp.X_post;
+    int mode = (need_x ? tr::kScoreImp : 0) | (need_c ? tr::kScoreSim : 0);
+    if (need_x && (c->p.flags & TR_FLAG_SHANNON)) mode |= tr::kScoreShannon;
 
     const int64_t row_bytes = (int64_t)c->p.D * c->eb;
     const int64_t rowc_bytes = (int64_t)c->Dc * c->eb;
@@ -536,7 +426,7 @@ tr_status tr_reduce(tr_ctx* c, const void* X, const void* X_pre, const void* X_p
                     const int32_t* N, const int32_t* K, void* out, int32_t* out_idx,
                     uint8_t* out_src, float* out_h2, float* out_s, void* stream)
 {
-    g_err.clear();
+    clear_error();
     ReduceCall r;
     r.X = X;
     r.X_pre = X_pre;
@@ -557,7 +447,7 @@ tr_status tr_reduce_given_s(tr_ctx* c, const void* X, const float* key_s, int32_
                             const int32_t* K, void* out, int32_t* out_idx, uint8_t* out_src, float* out_h2,
                             void* stream)
 {
-    g_err.clear();
+    clear_error();
     if (!key_s) return fail(TR_EINVAL, "key_s must be non-NULL");
     ReduceCall r;
     r.X = X;
@@ -577,7 +467,7 @@ tr_status tr_reduce_project(tr_ctx* c, const void* X, const void* X_pre, const v
                             const int32_t* N, const int32_t* K, const void* W, int64_t ldw, int32_t Nout,
                             void* out, int32_t* out_idx, uint8_t* out_src, void* stream)
 {
-    g_err.clear();
+    clear_error();
     if (!W) return fail(TR_EINVAL, "W must be non-NULL");
     ReduceCall r;
     r.X = X;
@@ -600,7 +490,7 @@ tr_status tr_gemm_bf16(tr_ctx* c, const void* A, int64_t lda, const int32_t* a_r
                        const void* B, int64_t ldb, void* C, int64_t ldc, int32_t M, int32_t N, int32_t K,
                        void* stream)
 {
-    g_err.clear();
+    clear_error();
     if (!c) return fail(TR_EINVAL, "ctx is NULL");
     if (M < 0) return fail(TR_EINVAL, "M must be >= 0");
     if (!tr::gemm_shape_ok(M, N, K))
@@ -633,7 +523,7 @@ tr_status tr_gemm_bf16(tr_ctx* c, const void* A, int64_t lda, const int32_t* a_r
 tr_status tr_mlp_out_cos(tr_ctx* c, const void* Hact, int64_t ldh, const void* W2, int64_t ldw,
                          const void* X_pre, void* X_post, int32_t M, int32_t Hd, float* key_s, void* stream)
 {
-    g_err.clear();
+    clear_error();
     if (!c) return fail(TR_EINVAL, "ctx is NULL");
     if (c->p.dtype != TR_BF16) return fail(TR_EUNSUPPORTED, "tr_mlp_out_cos needs a bf16 context");
     if (!c->cos_part) return fail(TR_EUNSUPPORTED, "tr_mlp_out_cos needs Dc %% 128 == 0 (Dc = %d)", c->Dc);
@@ -671,7 +561,7 @@ tr_status tr_mlp_out_cos(tr_ctx* c, const void* Hact, int64_t ldh, const void* W
 tr_status tr_read_bandwidth(const void* const* p, const int64_t* bytes, int32_t n, uint32_t* sink,
                             int32_t sink_words, void* stream)
 {
-    g_err.clear();
+    clear_error();
     if (n < 1 || n > tr::kReadBuffers || !p || !bytes)
         return fail(TR_EINVAL, "n must be in [1, %d] with host arrays p and bytes", tr::kReadBuffers);
     int64_t total = 0;
@@ -691,7 +581,7 @@ tr_status tr_read_bandwidth(const void* const* p, const int64_t* bytes, int32_t 
 tr_status tr_score(tr_ctx* c, const void* X, const void* X_pre, const void* X_post, int64_t rows,
                    float* key_imp, float* key_s, float* out_h2, void* stream)
 {
-    g_err.clear();
+    clear_error();
     if (!c) return fail(TR_EINVAL, "ctx is NULL");
     if (rows < 0) return fail(TR_EINVAL, "rows must be >= 0");
     if (rows == 0) return TR_OK;
@@ -703,9 +593,9 @@ tr_status tr_score(tr_ctx* c, const void* X, const void* X_pre, const void* X_po
         return fail(TR_EINVAL, "X_pre, X_post and key_s go together");
     const uintptr_t em = (uintptr_t)c->eb - 1;
     if (((uintptr_t)X | (uintptr_t)X_pre | (uintptr_t)X_post) & em)
-        return fail(TR_EINVAL, "tensor base pointers must be aligned to the element size");
+        return fail(TR_EUNSUPPORTED, "X, X_pre and X_post must be aligned to the element size (%d bytes)", c->eb);
     if (((uintptr_t)key_imp | (uintptr_t)key_s | (uintptr_t)out_h2) & 3u)
-        return fail(TR_EINVAL, "score outputs must be 4-byte aligned");
+        return fail(TR_EUNSUPPORTED, "score outputs must be 4-byte aligned");
     const int64_t row_bytes = (int64_t)c->p.D * c->eb;
     const int64_t rowc_bytes = (int64_t)c->Dc * c->eb;
     const bool vec = aligned16(X) && aligned16(X_pre) && aligned16(X_post) && row_bytes % 16 == 0 &&
@@ -734,7 +624,7 @@ tr_status tr_score(tr_ctx* c, const void* X, const void* X_pre, const void* X_po
 tr_status tr_select(tr_ctx* c, const float* key_imp, const float* key_s, int32_t B, const int32_t* N,
                     const int32_t* K, int32_t* out_idx, uint8_t* out_src, void* stream)
 {
-    g_err.clear();
+    clear_error();
     if (!c) return fail(TR_EINVAL, "ctx is NULL");
     Plan pl;
     tr_status st = check_ctx_plan(c, B, N, K, pl);
@@ -742,7 +632,7 @@ tr_status tr_select(tr_ctx* c, const float* key_imp, const float* key_s, int32_t
     if (B == 0) return TR_OK;
     if (!key_imp || !key_s || !out_idx) return fail(TR_EINVAL, "key_imp, key_s and out_idx must be non-NULL");
     if (((uintptr_t)key_imp | (uintptr_t)key_s | (uintptr_t)out_idx) & 3u)
-        return fail(TR_EINVAL, "key and index arrays must be 4-byte aligned");
+        return fail(TR_EUNSUPPORTED, "key and index arrays must be 4-byte aligned");
     DeviceGuard g(c->device);
     if (!g.ok) return fail(TR_EDEVICE, "hipSetDevice(%d) failed", c->device);
     hipError_t e = run_select(c, pl, key_imp, key_s, out_idx, out_src, nullptr, static_cast<hipStream_t>(stream));

@@ -6,20 +6,12 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "tr_plan.h"
 #include "tr_score.h"
 
 namespace tr {
 
 // ---- per-image selection (top-K1, ordered remainder, sort, stride) --------
-struct ImageDesc {
-    int32_t row_off;     // first row of the image in the packed batch
-    int32_t n;           // tokens
-    int32_t k1;          // Stage I budget
-    int32_t k2;          // Stage II budget
-    int32_t t;           // stride (>= 1 when k2 > 0)
-    int32_t out_off;     // first output slot
-};
-
 constexpr int kMaxDescPerLaunch = 32;
 
 struct SelectArgs {

@@ -16,8 +16,22 @@
 // factor 2 of c (near-uniform rows), and M2 = sum d^2 - (sum d)^2 / D has
 // little cancellation because c lies close to m.
 //
+// Range: both scores are invariant to scaling a row by a positive constant
+// (Eq. 3 divides by sum |x|, Eq. 6 by both norms), so X is scored as
+// |x| 2^-e with 2^e the binade of the probe mean: the power of two is applied
+// by the same fused multiply-add that subtracts the shift (exact for normal
+// values, no extra instruction), and the sums of squares stay far from fp32
+// overflow and underflow whatever the row's magnitude.  A row whose probe
+// mean lies outside [2^-120, 2^120] (an all-zero probe included) or whose
+// scaled sums leave [0, 2^100] is scored again from a second read of its
+// bytes, scaled from its exact maximum |x| and shifted by its exact mean.
+//
 // Eq. (6): fp32 sums of x'x'', x'^2 and x''^2 (bf16 rows: hardware bf16 dot
-// products of element pairs, accumulated in fp32).
+// products of element pairs, accumulated in fp32), unscaled.  When both
+// squared norms lie in [2^-60, FLT_MAX], products that underflow (or
+// denormal inputs) move s by less than 2^-40 and nothing overflowed; any
+// other row is scored again from a second read, each of x' and x'' scaled by
+// the power of two of its own maximum |x|, in fp32 fused multiply-adds.
 //
 // Lane partial sums are combined by a fixed DPP scan tree (the total is read
 // from lane 63 into every lane) and lane 0 writes the results.
@@ -38,8 +52,7 @@
 // refer to the same effective shift 1 / (1/c) and e keeps full relative
 // accuracy for near-uniform rows.  The terms are summed in base-2 units
 // (e / ln 2 and g / ln 2), which saves a multiply per element; the row's sum
-// is scaled by ln 2 once.  A row whose probe mean is 0 uses the plain
-// form H1 = log S - (sum |x| log |x|) / S instead.
+// is scaled by ln 2 once.
 #include "tr_score.h"
 #include "tr_wave.h"
 
@@ -117,18 +130,21 @@ __device__ __forceinline__ void load_partial(const char* row, int c, int m, floa
 }
 
 struct XAcc {
-    float sd;    // sum (|x| - c)
-    float sd2;   // sum (|x| - c)^2; Shannon: sum g(|x| / c) (or sum |x| log |x| when c = 0)
+    float sd;    // sum (|x| 2^-e - c)
+    float sd2;   // sum (|x| 2^-e - c)^2; Shannon: sum g(|x| 2^-e / c) / ln 2
 };
 
 struct CAcc {
     float dot, n1, n2;
 };
 
-__device__ __forceinline__ void x_chunk(XAcc& a, const float* v, int m, float c)
+// d = |x| 2^-e - c in one fused multiply-add (scale = 2^-e): the product is
+// exact for normal values, so d is the rounding of the exact scaled
+// difference, and for near-uniform rows exact (Sterbenz).
+__device__ __forceinline__ void x_chunk(XAcc& a, const float* v, int m, float c, float scale)
 {
     for (int k = 0; k < m; ++k) {
-        const float d = fabsf(v[k]) - c;
+        const float d = fmaf(fabsf(v[k]), scale, -c);
         a.sd += d;
         a.sd2 = fmaf(d, d, a.sd2);
     }
@@ -161,27 +177,17 @@ __device__ __forceinline__ float g2_shannon(float y, float u)
     return fabsf(y) < kShannonCut ? series : direct;
 }
 
-// Shannon partial sums over m elements for a row shift c > 0 (inv = 1/c;
-// inv2 = inv / ln 2 and delta2 = (c inv - 1) / ln 2 give y): sd as for CV^2,
-// sd2 = sum g(|x| / c) / ln 2.
-__device__ __forceinline__ void x_chunk_shannon(XAcc& a, const float* v, int m, float c, float inv,
-                                                float inv2, float delta2)
+// Shannon partial sums over m elements for a row shift c > 0 and scale
+// 2^-e (inv_u = 2^-e / c, u = |x| inv_u; inv2 = (1/c) / ln 2 and delta2 =
+// (c (1/c) - 1) / ln 2 give y): sd as for CV^2, sd2 = sum g(u) / ln 2.
+__device__ __forceinline__ void x_chunk_shannon(XAcc& a, const float* v, int m, float c, float scale,
+                                                float inv_u, float inv2, float delta2)
 {
     for (int k = 0; k < m; ++k) {
         const float ax = fabsf(v[k]);
-        const float d = ax - c;
+        const float d = fmaf(ax, scale, -c);
         a.sd += d;
-        a.sd2 += g2_shannon(fmaf(d, inv2, delta2), ax * inv);
-    }
-}
-
-// The same for a row whose probe mean is 0: sd = sum |x|, sd2 = sum |x| log |x|.
-__device__ __forceinline__ void x_chunk_shannon_plain(XAcc& a, const float* v, int m)
-{
-    for (int k = 0; k < m; ++k) {
-        const float ax = fabsf(v[k]);
-        a.sd += ax;
-        a.sd2 = fmaf(ax * kLn2, __builtin_amdgcn_logf(fmaxf(ax, 1e-30f)), a.sd2);
+        a.sd2 += g2_shannon(fmaf(d, inv2, delta2), ax * inv_u);
     }
 }
 
@@ -235,12 +241,133 @@ __device__ __forceinline__ Raw load_partial_raw(const char* row, int c, int m)
 
 __device__ __forceinline__ float wave_sum(float v) { return wave_sum_f32(v); }
 
-template <int V>
-__device__ __forceinline__ float abs_sum(const float* v, int m)
+// Element j of a row as fp32 (exact widening), for the re-read paths.
+template <bool BF16>
+__device__ __forceinline__ float elem(const char* row, int j)
 {
-    float s = 0.f;
-    for (int k = 0; k < m; ++k) s += fabsf(v[k]);
-    return s;
+    if constexpr (BF16) return __uint_as_float((uint32_t)reinterpret_cast<const uint16_t*>(row)[j] << 16);
+    else return reinterpret_cast<const float*>(row)[j];
+}
+
+// 2^-e for a positive m, e the exponent that puts m 2^-e in [0.5, 1), limited
+// to [-125, 126] so that 2^-e is a normal number (m 2^-e then lies in
+// [2^-24, 4) for every finite m > 0).
+__device__ __forceinline__ float binade_scale(float m)
+{
+    int e;
+    (void)frexpf(m, &e);
+    e = e < -125 ? -125 : (e > 126 ? 126 : e);
+    return ldexpf(1.f, -e);
+}
+
+__device__ __forceinline__ float wave_max_nonneg(float v)
+{
+    // non-negative floats order like their bit patterns
+    return __uint_as_float(wave_max_u32(__float_as_uint(v)));
+}
+
+__device__ __forceinline__ float wave_min_nonneg(float v)
+{
+    return __uint_as_float(~wave_max_u32(~__float_as_uint(v)));
+}
+
+// The row shift c of the scaled values and what the Shannon terms derive
+// from it (1/c and its rounding offset, folded with the scale).
+struct Shift {
+    float c, scale, inv_c, delta, inv_u, inv2, delta2;
+};
+
+__device__ __forceinline__ Shift make_shift(float c, float scale)
+{
+    Shift h;
+    h.c = c;
+    h.scale = scale;
+    h.inv_c = c > 0.f ? 1.f / c : 0.f;
+    h.delta = c > 0.f ? fmaf(c, h.inv_c, -1.f) : 0.f;
+    h.inv_u = h.inv_c * scale;
+    h.inv2 = h.inv_c * kInvLn2;
+    h.delta2 = h.delta * kInvLn2;
+    return h;
+}
+
+template <bool H1>
+__device__ __forceinline__ void x_accumulate(XAcc& xa, const float* v, int m, const Shift& h)
+{
+    if constexpr (H1) x_chunk_shannon(xa, v, m, h.c, h.scale, h.inv_u, h.inv2, h.delta2);
+    else x_chunk(xa, v, m, h.c, h.scale);
+}
+
+// Stage I sums of a row from a second read of its bytes: scaled by the power
+// of two of its exact maximum |x| and shifted by its exact scaled mean, so
+// that no term can overflow and none that matters underflows.  zero: every
+// element is 0 (or the row is not finite).
+struct XRow {
+    Shift h;
+    float sd, sd2;
+    bool zero;
+};
+
+template <bool BF16, bool H1>
+__device__ __noinline__ XRow x_reread(const char* row, int D, int lane)
+{
+    XRow r;
+    r.sd = r.sd2 = 0.f;
+    float mx = 0.f, mn = __builtin_inff();
+    for (int j = lane; j < D; j += kWave) {
+        const float a = fabsf(elem<BF16>(row, j));
+        mx = fmaxf(mx, a);
+        mn = fminf(mn, a);
+    }
+    const float rmax = wave_max_nonneg(mx);
+    const float rmin = wave_min_nonneg(mn);
+    r.zero = !(rmax > 0.f && rmax <= 3.40282347e38f);
+    if (r.zero) {
+        r.h = make_shift(0.f, 1.f);
+        return r;
+    }
+    // The values are scaled once here (exact: the results are normal or
+    // negligibly small), so the Shannon terms' 1/c is never folded with the
+    // scale, which for a tiny row could leave the fp32 range.
+    const float scale = binade_scale(rmax);
+    float sum = 0.f;
+    for (int j = lane; j < D; j += kWave) sum += fabsf(elem<BF16>(row, j)) * scale;
+    // (a row of one magnitude: that magnitude, exactly, as the shift)
+    r.h = make_shift(rmin == rmax ? rmax * scale : wave_sum(sum) / (float)D, 1.f);
+    XAcc xa{0.f, 0.f};
+    for (int j = lane; j < D; j += kWave) {
+        const float v = elem<BF16>(row, j) * scale;
+        x_accumulate<H1>(xa, &v, 1, r.h);
+    }
+    r.sd = wave_sum(xa.sd);
+    r.sd2 = wave_sum(xa.sd2);
+    return r;
+}
+
+// Eq. (6) from a second read of the two rows, each scaled by the power of two
+// of its own maximum |x| (s is invariant to both), in fp32 fused
+// multiply-adds.  A zero vector gives s = 0.
+template <bool BF16>
+__device__ __noinline__ float cos_reread(const char* pr, const char* qr, int Dc, int lane)
+{
+    float mp = 0.f, mq = 0.f;
+    for (int j = lane; j < Dc; j += kWave) {
+        mp = fmaxf(mp, fabsf(elem<BF16>(pr, j)));
+        mq = fmaxf(mq, fabsf(elem<BF16>(qr, j)));
+    }
+    const float xp = wave_max_nonneg(mp), xq = wave_max_nonneg(mq);
+    if (!(xp > 0.f) || !(xq > 0.f)) return 0.f;
+    const float sp = binade_scale(xp), sq = binade_scale(xq);
+    float dot = 0.f, n1 = 0.f, n2 = 0.f;
+    for (int j = lane; j < Dc; j += kWave) {
+        const float u = elem<BF16>(pr, j) * sp, v = elem<BF16>(qr, j) * sq;
+        dot = fmaf(u, v, dot);
+        n1 = fmaf(u, u, n1);
+        n2 = fmaf(v, v, n2);
+    }
+    dot = wave_sum(dot);
+    n1 = wave_sum(n1);
+    n2 = wave_sum(n2);
+    return dot / (sqrtf(n1) * sqrtf(n2));
 }
 
 template <bool BF16, bool VEC, int UNR, int MODE>
@@ -269,30 +396,35 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a)
     const bool tail_x = kX && (a.D % V) && (nfx & (kWave - 1)) == lane;
     const int mx = a.D - nfx * V;
     float tx[V];
+    tx[0] = 0.f;
     if (tail_x) load_partial<BF16>(xr, nfx, mx, tx);
 
     XAcc xa{0.f, 0.f};
     CAcc ca{0.f, 0.f, 0.f};
-    float c = 0.f, inv_c = 0.f, delta = 0.f, inv2 = 0.f, delta2 = 0.f;
-    // 1/c and its exact rounding offset for the Shannon terms.
-    auto set_shift = [&](float cc) {
-        c = cc;
-        if constexpr (kH1) {
-            inv_c = c > 0.f ? 1.f / c : 0.f;
-            delta = c > 0.f ? fmaf(c, inv_c, -1.f) : 0.f;
-            inv2 = inv_c * kInvLn2;
-            delta2 = delta * kInvLn2;
+    // The shift and scale from the probe mean (wave-uniform): the row is
+    // accumulated as |x| 2^-e with the probe mean in [0.5, 1) after scaling.
+    Shift sh = make_shift(0.f, 1.f);
+    bool fast_x = false;
+    // The probe is this lane's first m elements pv (lane 0 always has some).
+    // Its mean is the shift; when every probe element has one magnitude, that
+    // magnitude itself is (exact, so an exactly uniform row gets d = 0 and a
+    // key of exactly 0 whatever its magnitude).  Either way c is a mean or a
+    // value of a subset of the row, which bounds the cancellation in M2.
+    auto set_probe = [&](const float* pv, int m) {
+        const float ref = __uint_as_float(
+            (uint32_t)__builtin_amdgcn_readlane((int)__float_as_uint(fabsf(pv[0])), 0));
+        bool same = true;
+        float sum = 0.f;
+        for (int k = 0; k < m; ++k) {
+            sum += fabsf(pv[k]);
+            same = same && fabsf(pv[k]) == ref;
         }
+        const float c_raw = __all(same) ? ref : wave_sum(sum) / n_probe;
+        fast_x = c_raw >= 0x1p-120f && c_raw <= 0x1p120f;
+        const float scale = fast_x ? binade_scale(c_raw) : 1.f;
+        sh = make_shift(fast_x ? c_raw * scale : 0.f, scale);
     };
-    auto x_acc = [&](const float* v, int m) {
-        if constexpr (kH1) {
-            if (c > 0.f) x_chunk_shannon(xa, v, m, c, inv_c, inv2, delta2);   // c is wave-uniform
-            else x_chunk_shannon_plain(xa, v, m);
-        } else {
-            x_chunk(xa, v, m, c);
-        }
-    };
-    if (kX && nfx == 0) set_shift(wave_sum(tail_x ? abs_sum<V>(tx, mx) : 0.f) / n_probe);
+    if (kX && nfx == 0) set_probe(tx, tail_x ? mx : 0);
 
     for (int j0 = 0; j0 < nf; j0 += kWave * UNR) {   // same trip count for every lane
         Raw rx[UNR], rp[UNR], rq[UNR];
@@ -306,15 +438,19 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a)
             }
         }
         if (j0 == 0 && nfx > 0) {
-            float first = 0.f;
+            float v[V];
+            int m = 0;
             if (lane < nfx) {
-                float v[V];
                 unpack<BF16>(rx[0], v);
-                first = abs_sum<V>(v, V);
+                m = V;
             } else if (tail_x) {
-                first = abs_sum<V>(tx, mx);
+#pragma unroll
+                for (int k = 0; k < V; ++k) v[k] = tx[k];
+                m = mx;
+            } else {
+                v[0] = 0.f;
             }
-            set_shift(wave_sum(first) / n_probe);
+            set_probe(v, m);
         }
 #pragma unroll
         for (int u = 0; u < UNR; ++u) {
@@ -322,62 +458,74 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a)
             if (ci < nfx) {
                 float v[V];
                 unpack<BF16>(rx[u], v);
-                x_acc(v, V);
+                x_accumulate<kH1>(xa, v, V, sh);
             }
             if (ci < nfc) c_chunk<BF16>(ca, rp[u], rq[u]);
         }
     }
-    if (tail_x) x_acc(tx, mx);
+    if (tail_x) x_accumulate<kH1>(xa, tx, mx, sh);
     if (kC && a.Dc % V && (nfc & (kWave - 1)) == lane) {
         const int m = a.Dc - nfc * V;
         c_chunk<BF16>(ca, load_partial_raw<BF16>(pr, nfc, m), load_partial_raw<BF16>(qr, nfc, m));
     }
 
-    float sd = 0.f, sd2 = 0.f, dot = 0.f, n1 = 0.f, n2 = 0.f;
+    float sd = 0.f, sd2 = 0.f, s = 0.f;
+    bool zero_row = false;
     if constexpr (kX) {
         sd = wave_sum(xa.sd);
         sd2 = wave_sum(xa.sd2);
+        // Probe outside the window, or a scaled sum out of range (NaN too):
+        // score the row again from its maximum (a wave-uniform decision).
+        if (!(fast_x && sd2 <= 0x1p100f)) {
+            const XRow r = x_reread<BF16, kH1>(xr, a.D, lane);
+            sh = r.h;
+            sd = r.sd;
+            sd2 = r.sd2;
+            zero_row = r.zero;
+        }
     }
     if constexpr (kC) {
-        dot = wave_sum(ca.dot);
-        n1 = wave_sum(ca.n1);
-        n2 = wave_sum(ca.n2);
+        const float dot = wave_sum(ca.dot), n1 = wave_sum(ca.n1), n2 = wave_sum(ca.n2);
+        if (n1 >= 0x1p-60f && n2 >= 0x1p-60f && n1 <= 3.40282347e38f && n2 <= 3.40282347e38f)
+            s = dot / (sqrtf(n1) * sqrtf(n2));
+        else
+            s = cos_reread<BF16>(pr, qr, a.Dc, lane);
     }
 
     if (lane == 0) {
         float cv2 = 0.f, h2 = 0.f;
+        const float Df = (float)a.D;
+        const float mean = sh.c + sd / Df;   // of the scaled |x|
         if constexpr (kH1) {
             // cv2 holds the key KL = log D - H1, h2 holds H1.
-            const float Df = (float)a.D;
-            const float mean = c + sd / Df;
-            if (!(mean > 0.f)) {   // all-zero row: H1 = 0
+            if (zero_row || !(mean > 0.f)) {   // all-zero row: H1 = 0
                 cv2 = a.logD;
                 h2 = 0.f;
-            } else if (c > 0.f) {
-                const float rm1 = fmaf(sd / Df, inv_c, delta);   // r - 1
+            } else {
+                const float rm1 = fmaf(sd / Df, sh.inv_c, sh.delta);   // r - 1
                 const float r = 1.f + rm1;
-                const float dkl = kLn2 * (sd2 - Df * g2_shannon(rm1 * kInvLn2, r)) / r;
+                const float gr = Df * g2_shannon(rm1 * kInvLn2, r);
+                // sum g(u_j) >= D g(r) (Jensen), with equality only when every
+                // u_j is equal; for any other row the difference is at least
+                // about n_probe / (n_probe + D) of the sum.  A difference
+                // within the rounding of the sums ((D / 64 + 16) ulps) is an
+                // exactly uniform row, whose KL is 0 at any magnitude (such
+                // rows then tie exactly, as Eq. 3 makes them).
+                const float num = sd2 - gr;
+                const float thr = (Df * (1.f / kWave) + 16.f) * 0x1p-24f;
+                const float dkl = fabsf(num) <= thr * (sd2 + gr) ? 0.f : kLn2 * num / r;
                 cv2 = fmaxf(0.f, dkl / Df);
                 h2 = a.logD - cv2;
-            } else {   // probe mean 0: sd = sum |x|, sd2 = sum |x| log |x|
-                h2 = fmaxf(0.f, __logf(sd) - sd2 / sd);
-                cv2 = fmaxf(0.f, a.logD - h2);
             }
         } else if constexpr (kX) {
-            const float Df = (float)a.D;
-            const float mean = c + sd / Df;
             const float m2 = fmaxf(0.f, fmaf(-sd, sd / Df, sd2));
-            if (mean > 0.f) {
-                cv2 = (m2 / (mean * Df)) / mean;
-                h2 = a.logD - log1pf(cv2);
-            } else {   // all-zero row: H2 = 0, i.e. 1 + CV^2 = D
+            if (zero_row || !(mean > 0.f)) {   // all-zero row: H2 = 0, i.e. 1 + CV^2 = D
                 cv2 = Df - 1.f;
                 h2 = 0.f;
+            } else {
+                cv2 = (m2 / (mean * Df)) / mean;
+                h2 = a.logD - log1pf(cv2);
             }
-        }
-        float s = 0.f;
-        if constexpr (kC) {
-            if (n1 > 0.f && n2 > 0.f) s = dot / (sqrtf(n1) * sqrtf(n2));
         }
         if (a.key_imp) a.key_imp[row] = cv2;
         if (a.key_s) a.key_s[row] = s;

@@ -6,18 +6,26 @@ scale is O(1)).  Indices are compared exactly, except where the oracle's own
 score gap is inside the window an fp32 score error of TOL can cross:
 
 * P1  scores: |CV^2_gpu - CV^2| <= TOL CV^2 (+1e-12), |H2_gpu - H2| <=
-      TOL max(1, |H2|), |s_gpu - s| <= TOL max(1, |s|).  CV^2 = expm1(log D - H2)
+      TOL max(1, |H2|), |s_gpu - s| <= TOL max(S_FLOOR, |s|).  CV^2 = expm1(log D - H2)
       is the quantity the GPU ranks Stage I by (same order as H2).  Shannon
       variant: the key is KL = log D - H1 (+1e-11, the oracle's own rounding
       of a near-zero KL) and H1 takes H2's place.
 * P2  Stage I: the GPU's X^imp may differ from the oracle's only in tokens whose
-      oracle CV^2 lies within 2 TOL of the boundary value (the K1-th smallest);
-      each such token is a counted near-tie swap, anything else fails.
+      oracle CV^2 lies within the near-tie window of the boundary value (the
+      K1-th smallest); each such token is a counted near-tie swap, anything
+      else fails.
 * P3  Stage II, checked on the GPU's own X^imp so that a P2 swap cannot
       cascade: order X^rem by the oracle's (s, index); the GPU's j-th pick (in
       its own s order) must be the token at sorted position j t (floor(j R /
       K2) in the real-interval variant), or a token whose oracle s is within
-      2 TOL of it (a counted near tie).
+      the near-tie window of it (a counted near tie).
+      Windows: when the GPU's own scores are given, twice the largest score
+      error measured in this run (P1): the k-th smallest of perturbed values
+      moves by at most the largest perturbation, so a correctly ranked pick
+      and the expected token differ in oracle score by at most twice the
+      largest error, however crowded the scores are.  The window is never
+      wider than 2 TOL max(S_FLOOR, |s|) (CV^2: 2 TOL theta), and without the
+      GPU's scores it is that.
 * P4  output: K kept, strictly ascending, K1 from Stage I and K2 from Stage II,
       and out equal byte for byte to the kept rows of X.
 * P5  information only: raw mismatch count against the oracle's indices.
@@ -51,6 +59,16 @@ class Report:
 
     def ok(self) -> bool:
         return not self.failures
+
+    def near_ties_rare(self) -> bool:
+        """Near-tie excusals stay rare: at most max(2, images / 10) Stage I
+        swaps and max(4, picks / 100) Stage II near-tie picks.  Holds for the
+        benchmark workloads (fp32 scores flip an order only where the
+        oracle's fp64 gap is below ~1e-7); data crowded below that (thousands
+        of tokens whose s differ by less than the fp32 error) has legitimate
+        flips beyond it, which the measured-error windows still bound."""
+        return (self.stage1_swaps <= max(2, self.images // 10)
+                and self.stage2_near <= max(4, self.picks // 100))
 
     def summary(self) -> str:
         return ("images=%d tokens=%d max_rel_cv2=%.2e max_abs_h2=%.2e max_abs_s=%.2e "
@@ -87,8 +105,19 @@ def stage1_key(h: np.ndarray, D: int, entropy: int = 2) -> np.ndarray:
 
 
 # Absolute floor of the Stage I key comparison: the oracle's own rounding of
-# log D - H (fp64, sums over D terms) for keys near 0.
+# log D - H (fp64, sums over D terms) for keys near 0.  Renyi-2: CV^2 =
+# expm1(log D - H2) with H2 = -log(sum p^2) in fp64 has an absolute error of a
+# few ulps of log D (< 1e-14 for D <= 2^20), taken as 1e-12.  Shannon: KL =
+# log D - H1 with H1 = -sum p log p summed over D terms of size up to
+# log(D)/D; the fp64 sum's rounding is ~D eps log D (4096 terms: ~4e-12),
+# taken as 1e-11.
 KEY_FLOOR = {2: 1e-12, 1: 1e-11}
+
+# Scale floor of the s comparison: s lies in [-1, 1] and the synthetic
+# workloads' s values spread ~0.015 around their mean, so the relative
+# tolerance is taken on max(|s|, 1e-2): 1e-7 absolute near s = 0, still
+# ten times the largest s error measured on the GPU (8.7e-9).
+S_FLOOR = 1e-2
 
 
 def check(w, res, ref, cv2_gpu=None, tol: float = TOL, stride_mode: int = 0,
@@ -112,11 +141,14 @@ def check(w, res, ref, cv2_gpu=None, tol: float = TOL, stride_mode: int = 0,
         bad = np.nonzero(dh > tol * np.maximum(1.0, np.abs(h2o)))[0]
         if bad.size:
             rep.failures.append("P1 H2 outside tolerance at rows %s" % bad[:8].tolist())
+    s_err = None     # largest |s_gpu - s| of this run, when the GPU's s is given
+    key_err = None   # largest |key_gpu - key| likewise
     if res.s is not None:
         sg = res.s.double().cpu().numpy()
         ds = np.abs(sg - so)
         rep.max_abs_s = float(ds.max(initial=0))
-        bad = np.nonzero(ds > tol * np.maximum(1.0, np.abs(so)))[0]
+        s_err = rep.max_abs_s
+        bad = np.nonzero(ds > tol * np.maximum(S_FLOOR, np.abs(so)))[0]
         if bad.size:
             rep.failures.append("P1 s outside tolerance at rows %s" % bad[:8].tolist())
     if cv2_gpu is not None:
@@ -124,6 +156,7 @@ def check(w, res, ref, cv2_gpu=None, tol: float = TOL, stride_mode: int = 0,
         dc = np.abs(cg - cv2o)
         rel = dc / np.maximum(cv2o, 1e-300)
         rep.max_rel_cv2 = float(np.where(cv2o > 0, rel, 0).max(initial=0))
+        key_err = float(dc.max(initial=0))
         bad = np.nonzero(dc > tol * cv2o + floor)[0]
         if bad.size:
             rep.failures.append("P1 CV^2 outside tolerance at rows %s" % bad[:8].tolist())
@@ -162,6 +195,8 @@ def check(w, res, ref, cv2_gpu=None, tol: float = TOL, stride_mode: int = 0,
             order = np.lexsort((np.arange(n), c))
             theta = c[order[K1 - 1]]
             win = 2 * tol * theta + 2 * floor
+            if key_err is not None:
+                win = min(win, 2 * key_err + 2 * floor)
             if K1 < n and abs(c[order[K1]] - theta) <= win:
                 rep.stage1_windows += 1
             diff = np.setxor1d(imp_g, imp_o)
@@ -190,7 +225,9 @@ def check(w, res, ref, cv2_gpu=None, tol: float = TOL, stride_mode: int = 0,
             mism = np.nonzero(div != expect)[0]
             if mism.size:
                 gap = np.abs(s_img[div[mism]] - s_img[expect[mism]])
-                lim = 2 * tol * np.maximum(1.0, np.abs(s_img[expect[mism]]))
+                lim = 2 * tol * np.maximum(S_FLOOR, np.abs(s_img[expect[mism]]))
+                if s_err is not None:
+                    lim = np.minimum(lim, 2 * s_err + 1e-15)
                 if np.any(gap > lim):
                     j = mism[np.argmax(gap - lim)]
                     rep.failures.append("P3 image %d: pick %d is token %d, want %d (s gap %.3e)"

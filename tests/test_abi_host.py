@@ -217,3 +217,61 @@ def test_last_error_is_per_thread():
     t.join()
     assert seen["failing"] != b""
     assert seen["quiet_before"] == b"" and seen["quiet_after"] == b""
+
+
+# ----------------------------------------------------------- host sanitizers
+
+def _sanitizer_flags():
+    return ["-O1", "-g", "-fsanitize=address,undefined", "-fno-sanitize-recover=all",
+            "-fno-omit-frame-pointer"]
+
+
+def test_host_planner_under_sanitizers(tmp_path):
+    """The host-only planner (tr_plan.cpp: parameter checks, Algorithm 1's
+    budget plan, the argument rules of a reduce call, the error buffer) built
+    on its own with the address and undefined-behaviour sanitizers and driven
+    over valid and invalid calls, batches above and below its inline storage."""
+    exe = tmp_path / "plan_driver"
+    src = [os.path.join(ROOT, "tests", "sanitize", "plan_driver.cpp"),
+           os.path.join(ROOT, "paper_2607_13500_amd", "csrc", "tr_plan.cpp")]
+    res = subprocess.run(["g++", "-std=c++17", "-Wall", "-Wextra", "-I", os.path.join(ROOT, "include")]
+                         + _sanitizer_flags() + ["-o", str(exe)] + src, capture_output=True, text=True)
+    if res.returncode != 0 and "asan" in (res.stderr or "").lower():
+        pytest.skip("no sanitizer runtime: " + res.stderr[-200:])
+    assert res.returncode == 0, res.stderr
+    run = subprocess.run([str(exe)], capture_output=True, text=True, timeout=120,
+                         env=dict(os.environ, ASAN_OPTIONS="detect_leaks=1"))
+    assert run.returncode == 0, run.stdout + run.stderr
+    assert "planner ok" in run.stdout
+
+
+def test_check_reduce_states_the_alignment_rule():
+    """tr_check_reduce (host-only, no device) applies tr_reduce's argument
+    rules: a base not aligned to its element size is TR_EUNSUPPORTED, an
+    element-aligned one is accepted (scalar path), and inputs of a score the
+    call does not compute are neither required nor checked."""
+    lib = _lib.load()
+    N = (ctypes.c_int32 * 2)(100, 50)
+    K = (ctypes.c_int32 * 2)(10, 5)
+    g = 1 << 20   # addresses are inspected, never dereferenced
+    for dtype, e in ((_lib.TR_BF16, 2), (_lib.TR_FP32, 4)):
+        p = _lib.Params(D=64, Dc=0, dtype=dtype, max_images=0, max_tokens=0, max_N=0, flags=0,
+                        lam=1.0 / 3.0, keep_ratio=0.0)
+
+        def chk(X=g, P=g, Q=g, out=g, idx=g, h2=None, s=None):
+            return lib.tr_check_reduce(ctypes.byref(p), X, P, Q, 2, N, K, out, idx, None, h2, s)
+
+        assert chk() == _lib.TR_OK
+        assert chk(X=g + e, P=g + 3 * e, out=g + e) == _lib.TR_OK
+        for bad in (dict(X=g + 1), dict(P=g + 1), dict(Q=g + 1), dict(out=g + 1), dict(idx=g + 2),
+                    dict(h2=g + 2), dict(s=g + 2)):
+            assert chk(**bad) == _lib.TR_EUNSUPPORTED, bad
+            assert b"aligned" in lib.tr_last_error()
+        if dtype == _lib.TR_FP32:
+            assert chk(X=g + 2) == _lib.TR_EUNSUPPORTED
+        for missing in (dict(X=None), dict(P=None), dict(Q=None), dict(out=None), dict(idx=None)):
+            assert chk(**missing) == _lib.TR_EINVAL, missing
+        p.lam = 1.0
+        assert chk(P=None, Q=None) == _lib.TR_OK
+        assert chk(P=g + 1, Q=g + 1) == _lib.TR_OK
+        assert chk(P=None, Q=None, s=g) == _lib.TR_EINVAL       # asking for s needs the states

@@ -193,6 +193,7 @@ def test_fused_mlp_module_parity():
     rep = parity.check(wd, res, ref)
     print("   ", rep.summary(), flush=True)
     assert rep.ok(), rep.failures[:5]
+    assert rep.near_ties_rare(), rep.summary()
     r.close()
 
 
@@ -224,6 +225,7 @@ def test_reduce_project_parity(name, kw, nout):
     # the selection itself against the oracle (the gather path's parity)
     rep = parity.check(w, base, parity.oracle_reference(w))
     assert rep.ok(), rep.failures[:5]
+    assert rep.near_ties_rare(), rep.summary()
     r.close()
 
 

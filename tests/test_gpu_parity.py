@@ -45,6 +45,7 @@ def run_and_check(w, *, use_keep_ratio=False, tol=parity.TOL):
     rep = parity.check(w, res, ref, cv2_gpu=cv2, tol=tol)
     print("   ", w.name, rep.summary(), flush=True)
     assert rep.ok(), rep.failures[:5]
+    assert rep.near_ties_rare(), rep.summary()
     r.close()
     return rep, res
 
@@ -138,6 +139,128 @@ def test_degenerate_rows(D, Dc, dtype):
         assert abs(h2[2] - math.log(D)) < 1e-5 * math.log(D)        # uniform magnitude
     assert s[4] == 0.0 and s[5] == 0.0                              # zero-norm states
     assert abs(s[6] + 1.0) < 1e-6                                   # cos(x, -2x) = -1
+
+
+# Magnitudes where fp32 squares of the raw values underflow or overflow.
+SCALES = [1e-30, 1e-20, 1e-19, 1e18, 1e30]
+
+
+def _magnitude_workload(D, Dc, dtype, n=240, seed=9):
+    """Rows far from O(1): X near-uniform and Gaussian at every scale of SCALES
+    and at 1e37 (the probe's sum overflows fp32) and 1e-40 (denormal values);
+    rows mixing magnitudes (a block of 1e25 after O(1) values, a zero probe
+    before 1e-30 values, values spread log-uniformly over 1e-30..1e30); and
+    x', x'' Gaussian or nearly parallel with every pair of scales, scaled
+    independently, plus norms so small that their squares underflow."""
+    g = torch.Generator().manual_seed(seed)
+    f64 = dict(dtype=torch.float64)
+    X = torch.randn(n, D, generator=g, **f64)
+    P = torch.randn(n, Dc, generator=g, **f64)
+    # per-row noise levels spread s over (0.3, 1): distinct s values, so that
+    # the selection's near ties stay rare
+    sigma = 0.2 + 2.8 * torch.rand(n, 1, generator=g, **f64)
+    Q = P + sigma * torch.randn(n, Dc, generator=g, **f64)
+    eps = 10.0 ** (-2.5 + 2 * torch.rand(n, generator=g, **f64))
+    xs = []
+    for sc in SCALES + [1e37, 1e-40]:
+        xs.append(("gauss", sc))
+        xs.append(("near_uniform", sc))
+    xs += [("spike", 1.0), ("zero_probe", 1e-30), ("log_uniform", 1.0)]
+    cs = []
+    for sp in SCALES:
+        for sq in SCALES:
+            cs.append(("indep", sp, sq))
+            cs.append(("parallel", sp, sq))
+    cs += [("indep", 1e-35, 1e-35), ("indep", 1e-40, 1.0), ("parallel", 1e-38, 1e30), ("indep", 1e36, 1e36)]
+    for r in range(n):
+        kind, sc = xs[r % len(xs)]
+        if kind == "gauss":
+            X[r] *= sc
+        elif kind == "near_uniform":   # (1e-2: still distinct rows in bf16 at D = 37)
+            X[r] = sc * 1.3 * (1 + 1e-2 * torch.randn(D, generator=g, **f64))
+        elif kind == "spike":
+            X[r, D // 2:] *= 1e25
+        elif kind == "zero_probe":
+            X[r] *= sc
+            X[r, :min(D, 512)] = 0
+        elif kind == "log_uniform":
+            X[r] = torch.sign(X[r]) * 10.0 ** (60 * torch.rand(D, generator=g, **f64) - 30)
+        ck, sp, sq = cs[r % len(cs)]
+        if ck == "parallel":   # s from 1 - 5e-6 to about 0.95
+            Q[r] = P[r] * (1 + eps[r] * torch.randn(Dc, generator=g, **f64))
+        P[r] *= sp
+        Q[r] *= sq
+    cast = lambda t: t.to(dtype).to(DEV).contiguous()
+    return synth.Workload("magnitudes", cast(X), cast(P), cast(Q), [n], [40], synth.LAMBDA)
+
+
+@pytest.mark.parametrize("entropy", [2, 1])
+@pytest.mark.parametrize("D,Dc,dtype", [(4096, 4096, torch.bfloat16), (1024, 1024, torch.float32),
+                                        (4096, 3584, torch.float32), (37, 45, torch.bfloat16),
+                                        (600, 520, torch.bfloat16)])
+def test_extreme_magnitudes_match_the_oracle(D, Dc, dtype, entropy):
+    """Finite rows at magnitudes 1e-40..1e37 score like the fp64 oracle, token
+    by token (P1), and select like it (P2-P4): both scores are scale-invariant
+    and the kernel keeps its fp32 sums in range for any finite row."""
+    say("extreme magnitudes", D, Dc, dtype, "entropy", entropy)
+    w = _magnitude_workload(D, Dc, dtype)
+    r = reducer_for(w, shannon=(entropy == 1))
+    res = r.reduce(w.X, w.Xpre, w.Xpost, w.N, w.K, want_scores=True)
+    key, s2, h2 = r.score(w.X, w.Xpre, w.Xpost, want_h2=True)
+    torch.cuda.synchronize()
+    assert torch.equal(s2, res.s) and torch.equal(h2, res.h2)
+    assert torch.isfinite(key).all() and torch.isfinite(res.s).all() and torch.isfinite(res.h2).all()
+    rep = parity.check(w, res, parity.oracle_reference(w, entropy=entropy), cv2_gpu=key, entropy=entropy)
+    print("   ", w.name, "entropy", entropy, rep.summary(), flush=True)
+    assert rep.ok(), rep.failures[:5]
+    assert rep.near_ties_rare(), rep.summary()
+    r.close()
+
+
+@pytest.mark.parametrize("shannon", [False, True])
+@pytest.mark.parametrize("D,dtype", [(4096, torch.bfloat16), (37, torch.bfloat16), (1000, torch.float32)])
+def test_uniform_rows_tie_exactly_at_any_magnitude(D, dtype, shannon):
+    """Rows of one repeated magnitude (any signs) have the maximum entropy
+    log D exactly (Eq. 3 gives p = 1/D): their Stage I key is exactly 0 at
+    every magnitude, normal or not, so they tie and resolve by index."""
+    say("uniform rows", D, dtype, "shannon", shannon)
+    g = torch.Generator().manual_seed(D)
+    mags = [1.3e-40, 1e-30, 3.7e-20, 0.75, 1.1, 5e18, 2e30, 1e37]
+    X = torch.stack([m * torch.where(torch.rand(D, generator=g) < 0.5, -1.0, 1.0).double() for m in mags])
+    X = X.to(dtype).to(DEV).contiguous()
+    assert all(torch.unique(X[i].abs()).numel() == 1 for i in range(len(mags)))
+    r = tr_reducer(D, dtype, len(mags), shannon)
+    key, _, h = r.score(X, None, None, want_h2=True)
+    torch.cuda.synchronize()
+    assert torch.all(key == 0), key
+    assert torch.all(h == h[0]), h
+    r.close()
+
+
+def tr_reducer(D, dtype, rows, shannon=False):
+    import paper_2607_13500_amd as tr
+    return tr.Reducer(D, D, dtype, max_images=1, max_tokens=rows, max_N=rows, shannon=shannon)
+
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+def test_scores_are_invariant_to_power_of_two_scaling(dtype):
+    """Scaling a row of X, x' or x'' by 2^k (values staying normal) leaves
+    every score bit for bit unchanged: X is accumulated relative to the power
+    of two of its probe mean, and the cosine's sums scale exactly."""
+    D = Dc = 1024
+    say("power-of-two invariance", dtype)
+    w = _edge_workload(D, Dc, dtype, EDGE_KINDS, 150)
+    r = reducer_for(w)
+    key0, s0, h0 = r.score(w.X, w.Xpre, w.Xpost, want_h2=True)
+    # (the squared norms of x' and x'' stay inside the window where the
+    # cosine takes its one-pass form: 2^-60 .. 2^127)
+    for kx, kp, kq in ((-60, 10, -20), (40, -25, 25), (-20, -20, -20), (60, 0, 0)):
+        key, s, h = r.score((w.X * 2.0 ** kx).contiguous(), (w.Xpre * 2.0 ** kp).contiguous(),
+                            (w.Xpost * 2.0 ** kq).contiguous(), want_h2=True)
+        torch.cuda.synchronize()
+        assert torch.equal(key, key0) and torch.equal(h, h0), (kx, kp, kq)
+        assert torch.equal(s, s0), (kx, kp, kq)
+    r.close()
 
 
 def test_misaligned_pointers_give_identical_results():
@@ -286,6 +409,37 @@ def test_empty_batch_and_errors():
     r.close()
 
 
+def test_create_reports_enomem_and_keeps_nothing(monkeypatch):
+    """A device allocation failing inside tr_create (forced by the library's
+    TR_FAIL_ALLOC hook, for each of a bf16 context's six allocations) gives
+    TR_ENOMEM with *out == NULL, and frees what was already allocated."""
+    import ctypes
+    from paper_2607_13500_amd import _lib
+    say("tr_create allocation failures")
+    lib = _lib.load()
+    p = _lib.Params(D=4096, Dc=4096, dtype=_lib.TR_BF16, max_images=64, max_tokens=4_000_000, max_N=576,
+                    flags=0, lam=1.0 / 3.0, keep_ratio=0.0)
+    torch.cuda.synchronize()
+    free0, _ = torch.cuda.mem_get_info()
+    for k in range(1, 7):
+        monkeypatch.setenv("TR_FAIL_ALLOC", str(k))
+        for _ in range(4):
+            ctx = ctypes.c_void_p(1234)
+            st = lib.tr_create(ctypes.byref(p), ctypes.byref(ctx))
+            assert st == _lib.TR_ENOMEM, (k, st)
+            assert ctx.value is None
+            assert b"failed" in lib.tr_last_error()
+    monkeypatch.delenv("TR_FAIL_ALLOC")
+    torch.cuda.synchronize()
+    free1, _ = torch.cuda.mem_get_info()
+    # 24 failed creates; a leak of the allocations made before the failing one
+    # would keep at least 16 MB each (4M tokens x 4 B)
+    assert free0 - free1 < 32 << 20, (free0, free1)
+    ctx = ctypes.c_void_p()
+    assert lib.tr_create(ctypes.byref(p), ctypes.byref(ctx)) == _lib.TR_OK and ctx.value
+    lib.tr_destroy(ctx)
+
+
 def test_capacity_and_max_n():
     import paper_2607_13500_amd as tr
     cap = tr.capacity_N()
@@ -394,6 +548,7 @@ def test_reduce_is_ordered_on_the_callers_stream(name, kw):
     rep = parity.check(w, ref_run, parity.oracle_reference(w))
     print("   ", w.name, rep.summary(), flush=True)
     assert rep.ok(), rep.failures[:5]
+    assert rep.near_ties_rare(), rep.summary()
     r.close()
 
 
@@ -510,6 +665,7 @@ def test_lambda_extremes_skip_unused_scores(name, kw, lam):
     rep = parity.check(w, fast, parity.oracle_reference(w))
     print("   ", w.name, "lam", lam, rep.summary(), flush=True)
     assert rep.ok(), rep.failures[:5]
+    assert rep.near_ties_rare(), rep.summary()
     if lam == 1.0:
         assert rep.picks == 0
     r.close()
@@ -571,6 +727,7 @@ def test_shannon_variant_parity(name, kw):
     rep = parity.check(w, res, parity.oracle_reference(w, entropy=1), cv2_gpu=key, entropy=1)
     print("   ", w.name, "shannon", rep.summary(), flush=True)
     assert rep.ok(), rep.failures[:5]
+    assert rep.near_ties_rare(), rep.summary()
     assert rep.stage1_swaps <= max(1, rep.images // 10)
     r.close()
 
@@ -587,11 +744,13 @@ def test_shannon_degenerate_rows(D, Dc, dtype):
     rep = parity.check(w, res, parity.oracle_reference(w, entropy=1), cv2_gpu=key, entropy=1)
     print("   ", "edge shannon", rep.summary(), flush=True)
     assert rep.ok(), rep.failures[:5]
+    assert rep.near_ties_rare(), rep.summary()
     h1 = res.h2.cpu().numpy()
     if D > 1:
         assert h1[0] == 0.0 and h1[8] == 0.0                       # all-zero rows
         assert abs(h1[1]) < 1e-5                                    # one-hot (log D - KL in fp32)
         assert abs(h1[2] - math.log(D)) < 1e-5 * math.log(D)        # uniform magnitude
+        assert key[2].item() == 0.0 and key[10].item() == 0.0       # ... ties exactly: KL = 0
     r.close()
 
 
@@ -614,6 +773,7 @@ def test_stride_real_variant_parity(name, kw):
     rep = parity.check(w, res, ref, cv2_gpu=cv2, stride_mode=1)
     print("   ", w.name, "stride real", rep.summary(), flush=True)
     assert rep.ok(), rep.failures[:5]
+    assert rep.near_ties_rare(), rep.summary()
     assert rep.stage2_near <= max(4, rep.picks // 100)
     # the variant differs from Algorithm 1 wherever R / K2 is not an integer
     base = reducer_for(w).reduce(w.X, w.Xpre, w.Xpost, w.N, w.K)
@@ -658,6 +818,7 @@ def test_shannon_parity_full(name, kw, ratio):
     rep = parity.check(w, res, parity.oracle_reference(w, entropy=1), cv2_gpu=key, entropy=1)
     print("   ", w.name, "shannon", rep.summary(), flush=True)
     assert rep.ok(), rep.failures[:5]
+    assert rep.near_ties_rare(), rep.summary()
     assert rep.stage1_swaps <= max(2, rep.images // 10)
     r.close()
 
@@ -681,6 +842,7 @@ def test_variants_parity_full_llava(name, opt):
     rep = parity.check(w, res, ref, stride_mode=1 if stride_real else 0)
     print("   ", name, rep.summary(), flush=True)
     assert rep.ok(), rep.failures[:5]
+    assert rep.near_ties_rare(), rep.summary()
     assert rep.stage1_swaps <= 2 and rep.stage2_near <= max(4, rep.picks // 100)
     r.close()
 

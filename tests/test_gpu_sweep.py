@@ -68,5 +68,8 @@ def test_random_case_matches_oracle(seed, c):
     ref = parity.oracle_reference(w, stride_mode=stride_mode, entropy=entropy)
     rep = parity.check(w, res, ref, cv2_gpu=key1, stride_mode=stride_mode, entropy=entropy)
     print("   ", rep.summary(), flush=True)
+    # (no count bound: some cases crowd thousands of s values within the fp32
+    # error of each other; the measured-error windows of the protocol bound
+    # every excused pick instead)
     assert rep.ok(), rep.failures[:5]
     r.close()

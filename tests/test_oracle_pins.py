@@ -434,3 +434,62 @@ def test_select_rejects_invalid():
         oracle.select(np.zeros(4), np.zeros(4), 5, 0.5)
     with pytest.raises(ValueError):   # conditional X^imp of the wrong size
         oracle.select(np.zeros(4), np.zeros(4), 2, 0.5, given_imp=np.array([1, 1, 0, 0]))
+
+
+# ----------------------------------------------------------- host sanitizers
+
+def _asan_runtime():
+    import subprocess
+    path = subprocess.run(["gcc", "-print-file-name=libasan.so"], capture_output=True, text=True).stdout.strip()
+    return path if os.path.isabs(path) and os.path.exists(path) else None
+
+
+def _sanitized_oracle(tmp_path, source=None):
+    import subprocess
+    src = source or os.path.join(os.path.dirname(oracle.__file__), "altr_oracle.c")
+    lib = str(tmp_path / "liboracle_sanitized.so")
+    subprocess.check_call(["gcc", "-O1", "-g", "-std=c99", "-fPIC", "-shared", "-fsanitize=address,undefined",
+                           "-fno-sanitize-recover=all", "-fno-omit-frame-pointer", "-o", lib, src, "-lm"])
+    return lib
+
+
+def _pins_under_sanitizers(lib, select):
+    import subprocess
+    import sys
+    env = dict(os.environ, LD_PRELOAD=_asan_runtime(), ALTR_ORACLE_LIB=lib,
+               ASAN_OPTIONS="detect_leaks=0:verify_asan_link_order=0",
+               UBSAN_OPTIONS="halt_on_error=1:print_stacktrace=1")
+    # -s: a sanitizer report goes to the real stderr, not pytest's capture
+    return subprocess.run([sys.executable, "-u", "-m", "pytest", "-x", "-q", "-s", "-p", "no:cacheprovider", "-k",
+                           select, os.path.abspath(__file__)], capture_output=True, text=True, timeout=600, env=env,
+                          cwd=os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+
+
+def test_pins_hold_under_sanitizers(tmp_path):
+    """Every pin above, run against the oracle built with the address and
+    undefined-behaviour sanitizers (inputs come from numpy, whose buffers the
+    preloaded runtime guards): no out-of-bounds access, no undefined
+    arithmetic, same results."""
+    if _asan_runtime() is None:
+        pytest.skip("no address-sanitizer runtime")
+    res = _pins_under_sanitizers(_sanitized_oracle(tmp_path), "not sanitizer")
+    assert res.returncode == 0, res.stdout[-2000:] + res.stderr[-2000:]
+    assert " passed" in res.stdout
+
+
+def test_sanitizer_build_catches_an_out_of_bounds_read(tmp_path):
+    """The sanitized run is not vacuous: a copy of the oracle whose entropy
+    loop reads one element past the row is stopped by it."""
+    if _asan_runtime() is None:
+        pytest.skip("no address-sanitizer runtime")
+    text = open(os.path.join(os.path.dirname(oracle.__file__), "altr_oracle.c")).read()
+    start = text.index("double altr_oracle_renyi2(")
+    body = text[start:]
+    loop = body.index("j < D")
+    mutated = text[:start] + body[:loop] + "j <= D" + body[loop + len("j < D"):]
+    src = tmp_path / "altr_oracle_oob.c"
+    src.write_text(mutated)
+    res = _pins_under_sanitizers(_sanitized_oracle(tmp_path, str(src)), "h2_uniform")
+    assert res.returncode != 0
+    assert "AddressSanitizer" in res.stdout + res.stderr
+
