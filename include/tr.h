@@ -29,7 +29,8 @@
  * Memory: every pointer named "device" is HIP device memory on the device
  * that was current at tr_create; host arrays are read during the call only.
  * The caller owns all tensors; a context owns only the scratch it allocates
- * in tr_create.  No other call allocates memory.
+ * in tr_create.  No other call allocates memory (tr_reduce_noalloc works in a
+ * static device array of the library instead of a context's scratch).
  *
  * Layout: rows are packed back to back.  Image b's rows start at
  * sum_{b' < b} N[b'] in X, X_pre, X_post (and the score outputs), and its
@@ -279,6 +280,30 @@ tr_status tr_timing_read(tr_ctx* ctx, double* ms, int64_t* calls);
  * its contents are meaningless.  Needs no context. */
 tr_status tr_read_bandwidth(const void* const* p, const int64_t* bytes, int32_t n,
                             uint32_t* sink, int32_t sink_words, void* stream);
+
+/* ---- For callers that cannot allocate ------------------------------------
+ *
+ * tr_reduce without a context, for code that must not allocate device memory:
+ * work recorded under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc.  The problem statement comes in p as for tr_create (its
+ * capacity fields are optional limits, 0 = none); every other argument is as
+ * in tr_reduce, and the results are bit-identical to tr_reduce's with the same
+ * p.  The scratch is a static device array of the library: 6.4 MB on each GPU
+ * it runs on, held until the process ends, for at most TR_NOALLOC_MAX_TOKENS
+ * tokens (sum of N) in at most TR_NOALLOC_MAX_IMAGES images; larger calls
+ * return TR_EINVAL with nothing enqueued.  The call allocates no device or
+ * host memory; the first call on a device also enqueues one clear of the
+ * array (a kernel) on `stream`.  All calls on one GPU share that GPU's array
+ * and its contents persist between calls: calls that overlap on one GPU (two
+ * streams, two host threads) race and give undefined results, so callers
+ * serialise them. */
+#define TR_NOALLOC_MAX_TOKENS 524288
+#define TR_NOALLOC_MAX_IMAGES 256
+tr_status tr_reduce_noalloc(const tr_params* p, const void* X, const void* X_pre,
+                            const void* X_post, int32_t B, const int32_t* N,
+                            const int32_t* K, void* out, int32_t* out_idx,
+                            uint8_t* out_src, float* out_h2, float* out_s,
+                            void* stream);
 
 /* Release the context and its scratch (NULL is a no-op).  Freeing device
  * memory waits for the device to finish outstanding work first. */

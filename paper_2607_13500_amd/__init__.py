@@ -22,7 +22,7 @@ import torch
 from . import _lib
 from ._lib import Params
 
-__all__ = ["Reducer", "ReduceResult", "TRError", "plan", "capacity_N", "LAMBDA_PAPER"]
+__all__ = ["Reducer", "ReduceResult", "TRError", "plan", "capacity_N", "reduce_noalloc", "LAMBDA_PAPER"]
 
 LAMBDA_PAPER = 1.0 / 3.0   # 64 importance + 128 diversity of 192 (efficiency setting)
 
@@ -101,6 +101,34 @@ class ReduceResult(NamedTuple):
 
 def _flags(stride_real: bool, shannon: bool) -> int:
     return (_lib.TR_FLAG_STRIDE_REAL if stride_real else 0) | (_lib.TR_FLAG_SHANNON if shannon else 0)
+
+
+def reduce_noalloc(X: torch.Tensor, Xpre: Optional[torch.Tensor], Xpost: Optional[torch.Tensor],
+                   N: Sequence[int], K: Optional[Sequence[int]] = None, *, out: torch.Tensor,
+                   out_idx: torch.Tensor, out_src: Optional[torch.Tensor] = None,
+                   out_h2: Optional[torch.Tensor] = None, out_s: Optional[torch.Tensor] = None,
+                   lam: float = LAMBDA_PAPER, keep_ratio: Optional[float] = None,
+                   stride_real: bool = False, shannon: bool = False, stream=None) -> ReduceResult:
+    """tr_reduce_noalloc: the module without a context, working in the
+    library's static device scratch (at most TR_NOALLOC_MAX_TOKENS tokens in
+    TR_NOALLOC_MAX_IMAGES images).  Every output is the caller's: nothing is
+    allocated here or in the library.  D, Dc and the dtype come from X and
+    Xpre."""
+    if X.dtype not in _DTYPES or not X.is_cuda or X.dim() != 2 or not X.is_contiguous():
+        raise ValueError("X must be a contiguous [rows, D] float32 or bfloat16 tensor on a ROCm device")
+    if (Xpre is None) != (Xpost is None):
+        raise ValueError("Xpre and Xpost must both be given or both be None")
+    Dc = Xpre.shape[1] if Xpre is not None else X.shape[1]
+    p = _params(X.shape[1], Dc, X.dtype, lam, keep_ratio, 0, 0, 0, _flags(stride_real, shannon))
+    lib = _lib.load()
+    st = stream if stream is not None else torch.cuda.current_stream(X.device)
+    with torch.cuda.device(X.device):
+        status = lib.tr_reduce_noalloc(ctypes.byref(p), _ptr(X), _ptr(Xpre), _ptr(Xpost), len(N), _i32(N),
+                                       None if K is None else _i32(K), _ptr(out), _ptr(out_idx),
+                                       _ptr(out_src), _ptr(out_h2), _ptr(out_s),
+                                       ctypes.c_void_p(st.cuda_stream))
+    _check(status, "tr_reduce_noalloc")
+    return ReduceResult(out, out_idx, out_src, out_h2, out_s)
 
 
 class Reducer:

@@ -35,6 +35,8 @@ TR_OK, TR_EINVAL, TR_ENOMEM, TR_EUNSUPPORTED, TR_EDEVICE = range(5)
 TR_FP32, TR_BF16 = 0, 1
 TR_FLAG_STRIDE_REAL = 1
 TR_FLAG_SHANNON = 2
+TR_NOALLOC_MAX_TOKENS = 524288
+TR_NOALLOC_MAX_IMAGES = 256
 
 _lib = None
 
@@ -69,6 +71,8 @@ def load(build_if_missing: bool = True) -> ctypes.CDLL:
     lib.tr_reduce_project.restype = i32
     lib.tr_read_bandwidth.argtypes = [vp, vp, i32, vp, i32, vp]
     lib.tr_read_bandwidth.restype = i32
+    lib.tr_reduce_noalloc.argtypes = [P(Params), vp, vp, vp, i32, vp, vp, vp, vp, vp, vp, vp, vp]
+    lib.tr_reduce_noalloc.restype = i32
     lib.tr_check_reduce.argtypes = [P(Params), vp, vp, vp, i32, vp, vp, vp, vp, vp, vp, vp]
     lib.tr_check_reduce.restype = i32
     lib.tr_plan.argtypes = [P(Params), i32, vp, vp, vp, vp, vp, vp]

@@ -6,6 +6,8 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <atomic>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -641,3 +643,130 @@ tr_status tr_select(tr_ctx* c, const float* key_imp, const float* key_s, int32_t
 }
 
 }  // extern "C"
+
+// ---- tr_reduce without a context, for callers that cannot allocate ------------
+namespace {
+
+constexpr int64_t kStaticTokens = TR_NOALLOC_MAX_TOKENS;
+constexpr int32_t kStaticImages = TR_NOALLOC_MAX_IMAGES;
+constexpr size_t kStaticGselWords = (size_t)(kStaticTokens / 32) + 2 * (size_t)kStaticImages + 2;
+// Stage I keys, Stage II keys and kept-row list (a word per token each),
+// then the two split-selection bitmaps: 6.4 MB.
+constexpr size_t kStaticWords = 3 * (size_t)kStaticTokens + 2 * kStaticGselWords;
+static_assert(kStaticGselWords >= 2 + kStaticTokens / 32 + 2 * (size_t)kStaticImages,
+              "bitmap words of every image of a full call");
+
+// The scratch of tr_reduce_noalloc, one copy per device for the life of the
+// process.  In host code `scratch` names the symbol only; its device address
+// is taken once per device with hipGetSymbolAddress and used from then on.
+static __device__ __align__(256) uint32_t scratch[kStaticWords];
+
+__global__ __launch_bounds__(256) void fill_kernel(uint32_t* p, int64_t n, uint32_t v)
+{
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+        p[i] = v;
+}
+
+constexpr int kMaxDevices = 64;
+
+struct StaticDev {
+    uint32_t* ptr = nullptr;   // device address of `scratch` on this device
+    int lds = 0;
+    int cap_n = 0;
+    int cus = 256;
+};
+
+StaticDev g_static[kMaxDevices];
+std::atomic<int> g_static_ready[kMaxDevices];
+std::mutex g_static_mu;
+
+// Set-up on the first call on a device (that device current): the array's
+// address on this device, the selection's LDS limit, and one clear of the
+// array on the caller's stream (the split selection needs its bitmaps zero;
+// the keys start defined).  A fill kernel, not a memset, so that a first call
+// under graph capture records only kernels.
+tr_status static_setup(int dev, hipStream_t stream, const StaticDev*& out)
+{
+    if (dev < 0 || dev >= kMaxDevices) return fail(TR_EUNSUPPORTED, "device %d beyond %d devices", dev, kMaxDevices);
+    if (!g_static_ready[dev].load(std::memory_order_acquire)) {
+        std::lock_guard<std::mutex> lock(g_static_mu);
+        if (!g_static_ready[dev].load(std::memory_order_relaxed)) {
+            StaticDev sd;
+            void* ptr = nullptr;
+            hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+            if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+            sd.ptr = static_cast<uint32_t*>(ptr);
+            sd.lds = lds_limit_of(dev);
+            sd.cap_n = capacity_for(sd.lds);
+            if ((e = hipDeviceGetAttribute(&sd.cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess)
+                return hip_fail(e, "hipDeviceGetAttribute");
+            if ((e = tr::select_prepare(sd.lds)) != hipSuccess) return hip_fail(e, "hipFuncSetAttribute");
+            hipLaunchKernelGGL(fill_kernel, dim3(1024), dim3(256), 0, stream, sd.ptr, (int64_t)kStaticWords, 0u);
+            if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "scratch clear launch");
+            g_static[dev] = sd;
+            g_static_ready[dev].store(1, std::memory_order_release);
+        }
+    }
+    out = &g_static[dev];
+    return TR_OK;
+}
+
+}  // namespace
+
+extern "C" tr_status tr_reduce_noalloc(const tr_params* p, const void* X, const void* X_pre, const void* X_post,
+                                       int32_t B, const int32_t* N, const int32_t* K, void* out,
+                                       int32_t* out_idx, uint8_t* out_src, float* out_h2, float* out_s,
+                                       void* stream)
+{
+    clear_error();
+    tr_status st = check_params(p, false);
+    if (st != TR_OK) return st;
+    if (B > kStaticImages)
+        return fail(TR_EINVAL, "B = %d exceeds the %d images of the no-allocation scratch", B, kStaticImages);
+    if (B > 0 && N) {
+        int64_t rows = 0;
+        for (int32_t b = 0; b < B; ++b) rows += N[b] > 0 ? N[b] : 0;
+        if (rows > kStaticTokens)
+            return fail(TR_EINVAL, "sum of N = %lld exceeds the %lld tokens of the no-allocation scratch",
+                        (long long)rows, (long long)kStaticTokens);
+    }
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    const StaticDev* sd = nullptr;
+    if ((st = static_setup(dev, static_cast<hipStream_t>(stream), sd)) != TR_OK) return st;
+
+    // A context view on the device's copy of the array (allocates nothing).
+    tr_ctx c;
+    c.p = *p;
+    c.p.max_images = kStaticImages;
+    c.p.max_tokens = kStaticTokens;
+    c.p.max_N = p->max_N > 0 ? p->max_N : 0;
+    c.device = dev;
+    c.Dc = p->Dc ? p->Dc : p->D;
+    c.eb = elem_bytes(p->dtype);
+    c.lds_limit = sd->lds;
+    c.cap_n = sd->cap_n;
+    c.cus = sd->cus;
+    uint32_t* base = sd->ptr;
+    c.key_imp = reinterpret_cast<float*>(base);
+    c.key_s = reinterpret_cast<float*>(base + kStaticTokens);
+    c.rows = reinterpret_cast<int32_t*>(base + 2 * kStaticTokens);
+    c.gsel = base + 3 * kStaticTokens;
+    c.gimp = c.gsel + kStaticGselWords;
+
+    ReduceCall r;
+    r.X = X;
+    r.X_pre = X_pre;
+    r.X_post = X_post;
+    r.B = B;
+    r.N = N;
+    r.K = K;
+    r.out = out;
+    r.out_idx = out_idx;
+    r.out_src = out_src;
+    r.out_h2 = out_h2;
+    r.out_s = out_s;
+    r.stream = stream;
+    return reduce_impl(&c, r);
+}
