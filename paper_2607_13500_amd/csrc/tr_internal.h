@@ -27,8 +27,23 @@ struct SelectArgs {
     int32_t img0;           // index of the first image of this launch in the batch
     int32_t groups;         // workgroups per image (1, or more to split large images)
     int32_t stride_real;    // 1: X^div at floor(j R / K2) instead of j t
+    // Gather fused into the small-image selection (images of at most
+    // kSmallSelectN tokens): the kept rows of gX go to gout in output order.
+    const void* gX;         // [sum N] rows of grow_bytes, or nullptr: no fused gather
+    void* gout;             // [sum K] rows of grow_bytes
+    int64_t grow_bytes;
+    int32_t gvec;           // 1: 16-byte copies (bases and row pitch 16-byte aligned)
+    int32_t gelem;          // element bytes (2 or 4) of the element-wise copy
+    int32_t ggroups;        // workgroups per image of the small-image selection (>= 1)
     ImageDesc desc[kMaxDescPerLaunch];
 };
+
+// Images of at most this many tokens are selected one token per thread, and
+// can have their gather fused into the selection.
+constexpr int kSmallSelectN = 1024;
+// Workgroups per image of the small-image selection when it also gathers:
+// each repeats the (cheap) selection and copies a share of the kept rows.
+int select_small_groups(int images, int k_min, int cus);
 
 // Words of the split-image pick bitmaps for capacity (max_tokens, max_images).
 size_t select_gsel_words(int64_t max_tokens, int max_images);

@@ -1,5 +1,8 @@
-// Per-image selection (Algorithm 1 after the scores): one 1024-thread
-// workgroup per image, everything resident in LDS.
+// Per-image selection (Algorithm 1 after the scores), everything resident in
+// LDS.  Images of at most kSmallSelectN tokens take select_small_kernel (one
+// token per thread, both stages ranked in the same passes; described where
+// it is defined).  Larger images take select_kernel: one 1024-thread
+// workgroup per image, or several sharing the ranking of a large image.
 //
 // Keys are fp32 scores mapped to order-preserving u32 (-0 == +0).  Stage I
 // keeps the K1 smallest Stage I keys (ties: lower index); Stage II orders
@@ -1093,6 +1096,334 @@ __global__ __launch_bounds__(kThreads) void emit_kernel(SelectArgs a)
     emit(a, d, bimp, bsel, slots);
 }
 
+// ---- images of at most kSmallSelectN tokens: one token per thread ------------
+//
+// Both stages are ranked in the same passes.  Every token gets its exact rank
+// in (Stage I key, index) order and in (Stage II key, index) order among all N
+// tokens; X^imp is the ranks below K1, and a token of X^rem ranks in X^rem as
+// its Stage II rank minus the X^imp tokens ranked below it (read from a
+// bitmap of X^imp in Stage II rank order), which decides the stride picks.
+// Ranks come from value buckets and exact counting inside a bucket: bucket =
+// clamp(floor((v - lo) nb / (hi - lo)), 0, nb - 1) is non-decreasing in the
+// key, so rank = (tokens in lower buckets) + (members of the token's bucket
+// smaller in (key, index) order).  lo and hi are about the 1.5 % and 98.5 %
+// quantiles of a 64-key sample, so outliers (all-zero rows, zero-norm states)
+// land in the two end buckets instead of crowding the bulk into a few; when
+// the sample's range is not a finite positive float width, buckets are equal
+// ranges of the order-preserving key itself.  All keys equal: rank = index.
+// Phases are separated by eight workgroup barriers.  With a fused gather, G
+// workgroups share an image: each repeats the selection and copies every G-th
+// share of the kept rows (group 0 writes out_idx / out_src / out_rows).
+
+struct SmallLayout {
+    size_t hi, hs, si, ss, li, ls, samp, slots, misc, imps, kept, total;
+};
+
+__host__ __device__ inline SmallLayout small_layout(int T)
+{
+    SmallLayout L;
+    size_t o = 0;
+    L.hi = o;  o += 4 * (size_t)T;            // Stage I histogram, then cursors
+    L.hs = o;  o += 4 * (size_t)T;            // Stage II histogram, then cursors
+    L.si = o;  o += 4 * ((size_t)T + 1);      // Stage I bucket starts
+    L.ss = o;  o += 4 * ((size_t)T + 1);      // Stage II bucket starts
+    o = align_up(o, 16);
+    L.li = o;  o += 8 * (size_t)T;            // (key << 32 | index) in Stage I bucket order
+    L.ls = o;  o += 8 * (size_t)T;            // the same for Stage II
+    L.samp = o; o += 8 * 128;                 // 64-key samples of both keys, (key << 6 | k)
+    L.slots = o; o += 4 * 8 * kW;             // per-wavefront partial values
+    L.misc = o; o += 4 * 16;                  // broadcast slots
+    L.imps = o; o += 4 * 32;                  // X^imp bitmap in Stage II rank order
+    L.kept = o; o += 4 * (size_t)T;           // token of each output slot (fused gather)
+    L.total = o;
+    return L;
+}
+
+// Bucketing of one key over [lo, hi] (order keys) into nb buckets.
+struct Bucketing {
+    int32_t mode;      // 0: value buckets; 1: order-key buckets; 2: every key equal
+    float fmin, scale;
+    uint32_t kmin;
+    int32_t shift;
+};
+
+// kmin / kmax: the true range of the keys (order keys); value buckets need
+// every key to be a number (NaN keys lie outside [-inf, +inf] in key order).
+__device__ __forceinline__ Bucketing make_bucketing(uint32_t lo, uint32_t hi, uint32_t kmin, uint32_t kmax, int nb)
+{
+    Bucketing b;
+    b.mode = 2;
+    b.kmin = lo;
+    b.fmin = key_value(lo);
+    b.scale = 0.f;
+    b.shift = 0;
+    if (kmin == kmax) return b;
+    const bool no_nan = kmin >= 0x007fffffu && kmax <= 0xff800000u;
+    const float width = key_value(hi) - b.fmin;
+    const float scale = (float)nb / width;
+    if (no_nan && width > 0.f && width < 3.0e38f && scale < 3.0e38f) {
+        b.mode = 0;
+        b.scale = scale;
+        return b;
+    }
+    b.mode = 1;
+    const uint32_t span = hi - lo;
+    int sh = 0;
+    while (sh < 31 && (span >> sh) >= (uint32_t)nb) ++sh;
+    b.shift = sh;
+    return b;
+}
+
+// Non-decreasing in the key; always in [0, nb).
+__device__ __forceinline__ int bucket_of(const Bucketing& b, uint32_t k, int nb)
+{
+    if (b.mode == 0) {
+        const float x = (key_value(k) - b.fmin) * b.scale;   // NaN only if a key is NaN (then mode 1)
+        return x <= 0.f ? 0 : (x >= (float)(nb - 1) ? nb - 1 : (int)x);
+    }
+    if (b.mode == 1) {
+        if (k <= b.kmin) return 0;
+        const uint32_t q = (k - b.kmin) >> b.shift;
+        return q >= (uint32_t)nb ? nb - 1 : (int)q;
+    }
+    return 0;
+}
+
+// About the 1.5 % and 98.5 % quantiles of 64 sampled keys of an image (all
+// of them for N <= 64), computed by one wavefront without the workgroup:
+// lane k loads sample k (token floor(k N / 64)), the wave stages the samples
+// as distinct (key << 6 | k) values in its own LDS row, every lane ranks its
+// sample among the 64 (two per 16-byte broadcast read), and the lanes holding
+// ranks lo_rank and hi_rank publish their keys in out[0], out[1].
+__device__ __forceinline__ void sample_quantiles(const float* keys, int N, int lane, uint64_t* samp,
+                                                 uint32_t* out)
+{
+    const int st = N > kWave ? (int)(((int64_t)lane * N) >> 6) : lane;
+    const uint64_t mine = ((uint64_t)(st < N ? order_key(keys[st]) : 0xffffffffu) << 6) | (uint64_t)lane;
+    samp[lane] = mine;
+    // LDS operations of one wavefront complete in order: the row written
+    // above is visible to the reads below
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    const ulonglong2* sv = reinterpret_cast<const ulonglong2*>(samp);
+    int r = 0;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        ulonglong2 q[16];
+#pragma unroll
+        for (int j = 0; j < 16; ++j) q[j] = sv[16 * h + j];
+#pragma unroll
+        for (int j = 0; j < 16; ++j) r += (q[j].x < mine ? 1 : 0) + (q[j].y < mine ? 1 : 0);
+    }
+    const int lo_rank = N > kWave ? 1 : 0, hi_rank = N > kWave ? kWave - 2 : N - 1;
+    if (r == lo_rank) out[0] = (uint32_t)(mine >> 6);
+    if (r == hi_rank) out[1] = (uint32_t)(mine >> 6);
+}
+
+// Exact rank of `me` = (key << 32 | index) among the n > 1 members
+// list[beg, beg + n) of its bucket, plus beg (the tokens of lower buckets).
+__device__ __forceinline__ uint32_t rank_in(const uint64_t* list, uint32_t beg, uint32_t n, uint64_t me)
+{
+    const uint32_t end = beg + n;
+    uint32_t r = beg, j = beg;
+    for (; j + 4 <= end; j += 4) {
+        const uint64_t m0 = list[j], m1 = list[j + 1], m2 = list[j + 2], m3 = list[j + 3];
+        r += (m0 < me) + (m1 < me) + (m2 < me) + (m3 < me);
+    }
+    for (; j < end; ++j) r += list[j] < me ? 1u : 0u;
+    return r;
+}
+
+typedef uint32_t u32x4s __attribute__((ext_vector_type(4)));
+
+__global__ __launch_bounds__(kSmallSelectN) void select_small_kernel(SelectArgs a)
+{
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int T = (int)blockDim.x, nb = T, nw = T / kWave;
+    const int G = a.ggroups > 0 ? a.ggroups : 1;
+    const int local = (int)blockIdx.x / G, part = (int)blockIdx.x % G;
+    const Img d = image_of(a, local);
+    const int N = d.n, K1 = d.k1, K2 = d.k2, K = K1 + K2;
+    const int tid = (int)threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
+    const bool valid = tid < N;
+    const SmallLayout L = small_layout(T);
+    uint32_t* Hi = reinterpret_cast<uint32_t*>(smem + L.hi);
+    uint32_t* Hs = reinterpret_cast<uint32_t*>(smem + L.hs);
+    uint32_t* Si = reinterpret_cast<uint32_t*>(smem + L.si);
+    uint32_t* Ss = reinterpret_cast<uint32_t*>(smem + L.ss);
+    uint64_t* Li = reinterpret_cast<uint64_t*>(smem + L.li);
+    uint64_t* Ls = reinterpret_cast<uint64_t*>(smem + L.ls);
+    uint64_t* samp = reinterpret_cast<uint64_t*>(smem + L.samp);
+    uint32_t* slots = reinterpret_cast<uint32_t*>(smem + L.slots);
+    uint32_t* misc = reinterpret_cast<uint32_t*>(smem + L.misc);
+    uint32_t* imps = reinterpret_cast<uint32_t*>(smem + L.imps);
+    uint32_t* kept = reinterpret_cast<uint32_t*>(smem + L.kept);
+
+    // ---- keys, samples, per-wavefront ranges ----------------------------------
+    uint32_t ki = 0, ks = 0;
+    if (valid) {
+        ki = order_key(a.key_imp[d.row_off + tid]);
+        ks = order_key(a.key_s[d.row_off + tid]);
+    }
+    // the quantiles of both keys, by wavefronts 0 and 1 (0 alone for N <= 64)
+    if (w == 0) sample_quantiles(a.key_imp + d.row_off, N, lane, samp, &misc[0]);
+    if (w == (nw > 1 ? 1 : 0)) sample_quantiles(a.key_s + d.row_off, N, lane, samp + kWave, &misc[2]);
+    Hi[tid] = 0u;
+    Hs[tid] = 0u;
+    kept[tid] = 0xffffffffu;
+    if (tid < 32) imps[tid] = 0u;
+    {
+        const uint32_t nlo_i = wave_max_u32(valid ? ~ki : 0u), hi_i = wave_max_u32(valid ? ki : 0u);
+        const uint32_t nlo_s = wave_max_u32(valid ? ~ks : 0u), hi_s = wave_max_u32(valid ? ks : 0u);
+        if (lane == 0) {
+            slots[w] = nlo_i;
+            slots[kW + w] = hi_i;
+            slots[2 * kW + w] = nlo_s;
+            slots[3 * kW + w] = hi_s;
+        }
+    }
+    __syncthreads();   // B1
+    auto max_of = [&](const uint32_t* row) { return wave_max_u32(lane < nw ? row[lane] : 0u); };
+    const uint32_t kimin = ~max_of(slots), kimax = max_of(slots + kW);
+    const uint32_t ksmin = ~max_of(slots + 2 * kW), ksmax = max_of(slots + 3 * kW);
+    // Buckets over the sample quantiles (outliers clamp into the end buckets);
+    // the histogram's atomic returns each token's place within its bucket.
+    const Bucketing bi = make_bucketing(misc[0], misc[1], kimin, kimax, nb);
+    const Bucketing bs = make_bucketing(misc[2], misc[3], ksmin, ksmax, nb);
+    const int gi = valid ? bucket_of(bi, ki, nb) : 0;
+    const int gs = valid ? bucket_of(bs, ks, nb) : 0;
+    uint32_t li = 0, ls = 0;
+    if (valid) {
+        li = atomicAdd(&Hi[gi], 1u);
+        ls = atomicAdd(&Hs[gs], 1u);
+    }
+    __syncthreads();   // B2
+    // ---- bucket starts: thread t owns bucket t ----------------------------------
+    const uint32_t ci = Hi[tid], cs = Hs[tid];
+    const uint32_t inc_i = wave_scan_add(ci), inc_s = wave_scan_add(cs);
+    if (lane == kWave - 1) {
+        slots[4 * kW + w] = inc_i;
+        slots[5 * kW + w] = inc_s;
+    }
+    __syncthreads();   // B3
+    Si[tid] = inc_i - ci + sum_before(slots + 4 * kW, w, lane);
+    Ss[tid] = inc_s - cs + sum_before(slots + 5 * kW, w, lane);
+    if (tid == T - 1) {
+        Si[T] = (uint32_t)N;
+        Ss[T] = (uint32_t)N;
+    }
+    __syncthreads();   // B4
+    // ---- members of shared buckets listed; exact ranks ------------------------
+    const uint64_t me_i = ((uint64_t)ki << 32) | (uint32_t)tid;
+    const uint64_t me_s = ((uint64_t)ks << 32) | (uint32_t)tid;
+    uint32_t bi0 = 0, bi1 = 0, bs0 = 0, bs1 = 0;
+    if (valid) {
+        bi0 = Si[gi];
+        bi1 = Si[gi + 1];
+        bs0 = Ss[gs];
+        bs1 = Ss[gs + 1];
+        if (bi1 - bi0 > 1u) Li[bi0 + li] = me_i;
+        if (bs1 - bs0 > 1u) Ls[bs0 + ls] = me_s;
+    }
+    __syncthreads();   // B5
+    uint32_t ri = bi0, rs = bs0;
+    if (valid) {
+        if (bi.mode == 2) ri = (uint32_t)tid;
+        else if (bi1 - bi0 > 1u) ri = rank_in(Li, bi0, bi1 - bi0, me_i);
+        if (bs.mode == 2) rs = (uint32_t)tid;
+        else if (bs1 - bs0 > 1u) rs = rank_in(Ls, bs0, bs1 - bs0, me_s);
+        rs = rs < (uint32_t)N ? rs : (uint32_t)N - 1u;   // a rank below N in every case (memory safety)
+    }
+    const bool imp = valid && ri < (uint32_t)K1;
+    if (imp && K2 > 0) atomicOr(&imps[rs >> 5], 1u << (rs & 31));
+    __syncthreads();   // B6
+    // ---- stride picks on the rank in X^rem, union, output slots -------------------
+    // X^imp tokens ranked below rs: a wave scan of the bitmap words' counts
+    // (lane q holds word q), then the partial word.
+    const uint32_t wc = lane < 32 ? (uint32_t)__popc(imps[lane]) : 0u;
+    const uint32_t wex = wave_scan_add(wc) - wc;
+    const uint32_t wbelow = (uint32_t)__shfl((int)wex, (int)(rs >> 5));   // every lane takes part
+    bool pick = false;
+    if (valid && !imp && K2 > 0) {
+        const uint32_t below = wbelow + (uint32_t)__popc(imps[rs >> 5] & ((1u << (rs & 31)) - 1u));
+        const Stride sp{(uint32_t)d.t, (uint32_t)(N - K1), (uint32_t)K2, a.stride_real != 0};
+        pick = sp.picks(rs - below);
+    }
+    const bool sel = imp || pick;
+    const uint64_t bm = __ballot(sel);
+    if (lane == 0) slots[6 * kW + w] = (uint32_t)__popcll(bm);
+    __syncthreads();   // B7
+    const uint32_t slot = sum_before(slots + 6 * kW, w, lane) + (uint32_t)__popcll(bm & lanes_below(lane));
+    if (sel && slot < (uint32_t)K) {   // never more than K writes, whatever the keys
+        if (part == 0) {
+            const int o = d.out_off + (int)slot;
+            a.out_idx[o] = tid;
+            if (a.out_src) a.out_src[o] = imp ? 0 : 1;
+            if (a.out_rows) a.out_rows[o] = d.row_off + tid;
+        }
+        kept[slot] = (uint32_t)tid;
+    }
+    if (!a.gX) return;
+    __syncthreads();   // B8
+    // ---- fused gather: this group's share of the kept rows -------------------------
+    const int s0 = (int)(((int64_t)part * K) / G), s1 = (int)(((int64_t)(part + 1) * K) / G);
+    const char* X = static_cast<const char*>(a.gX);
+    char* out = static_cast<char*>(a.gout);
+    const int64_t rb = a.grow_bytes;
+    if (a.gvec) {
+        // Chunk j = r * cpr + c of the share, walked with (r, c) carried
+        // from step to step (no division per chunk).
+        const uint32_t cpr = (uint32_t)(rb / 16);
+        const uint32_t rows = (uint32_t)(s1 - s0);
+        const uint32_t qT = (uint32_t)T / cpr, mT = (uint32_t)T % cpr;
+        uint32_t r = (uint32_t)tid / cpr, c = (uint32_t)tid % cpr;
+        constexpr int kUnr = 8;
+        while (r < rows) {
+            u32x4s v[kUnr];
+            uint32_t rr[kUnr], cc[kUnr];
+#pragma unroll
+            for (int u = 0; u < kUnr; ++u) {
+                rr[u] = r;
+                cc[u] = c;
+                if (r < rows) {
+                    const uint32_t k = kept[s0 + (int)r];
+                    const uint32_t tk = k < (uint32_t)N ? k : 0u;   // always a filled slot
+                    v[u] = __builtin_nontemporal_load(
+                        reinterpret_cast<const u32x4s*>(X + (int64_t)(d.row_off + (int)tk) * rb) + c);
+                }
+                c += mT;
+                r += qT;
+                if (c >= cpr) {
+                    c -= cpr;
+                    ++r;
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < kUnr; ++u) {
+                if (rr[u] < rows)
+                    __builtin_nontemporal_store(
+                        v[u], reinterpret_cast<u32x4s*>(out + (int64_t)(d.out_off + s0 + (int)rr[u]) * rb) + cc[u]);
+            }
+        }
+    } else if (a.gelem == 2) {
+        const int64_t epr = rb / 2;
+        for (int r = s0; r < s1; ++r) {
+            const uint32_t tk = kept[r] < (uint32_t)N ? kept[r] : 0u;
+            const uint16_t* src = reinterpret_cast<const uint16_t*>(X + (int64_t)(d.row_off + (int)tk) * rb);
+            uint16_t* dst = reinterpret_cast<uint16_t*>(out + (int64_t)(d.out_off + r) * rb);
+            for (int64_t c = tid; c < epr; c += T) dst[c] = src[c];
+        }
+    } else {
+        const int64_t epr = rb / 4;
+        for (int r = s0; r < s1; ++r) {
+            const uint32_t tk = kept[r] < (uint32_t)N ? kept[r] : 0u;
+            const uint32_t* src = reinterpret_cast<const uint32_t*>(X + (int64_t)(d.row_off + (int)tk) * rb);
+            uint32_t* dst = reinterpret_cast<uint32_t*>(out + (int64_t)(d.out_off + r) * rb);
+            for (int64_t c = tid; c < epr; c += T) dst[c] = src[c];
+        }
+    }
+}
+
 }  // namespace
 
 int select_threads(int nmax)
@@ -1130,13 +1461,34 @@ hipError_t select_prepare(int lds_limit)
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&select_kernel),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, lds_limit);
     if (e != hipSuccess) return e;
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(&select_small_kernel),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, lds_limit);
+    if (e != hipSuccess) return e;
     return hipFuncSetAttribute(reinterpret_cast<const void*>(&emit_kernel),
                                hipFuncAttributeMaxDynamicSharedMemorySize, lds_limit);
+}
+
+int select_small_groups(int images, int k_min, int cus)
+{
+    // enough workgroups to keep every compute unit copying, at most one per
+    // kept row and 16 per image
+    int g = (2 * cus + images - 1) / (images > 0 ? images : 1);
+    if (g > 16) g = 16;
+    if (g > k_min) g = k_min;
+    return g < 1 ? 1 : g;
 }
 
 hipError_t launch_select(const SelectArgs& a, int nmax, hipStream_t s)
 {
     if (a.nimg <= 0) return hipSuccess;
+    if (nmax <= kSmallSelectN) {
+        const int T = ((nmax > kWave ? nmax : kWave) + kWave - 1) / kWave * kWave;
+        const int G = a.gX && a.ggroups > 0 ? a.ggroups : 1;
+        SelectArgs b = a;
+        b.ggroups = G;
+        hipLaunchKernelGGL(select_small_kernel, dim3(a.nimg * G), dim3(T), small_layout(T).total, s, b);
+        return hipGetLastError();
+    }
     const size_t lds = launch_lds(nmax);
     const int groups = a.groups > 0 ? a.groups : 1;
     hipLaunchKernelGGL(select_kernel, dim3(a.nimg * groups), dim3(kThreads), lds, s, a);
