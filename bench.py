@@ -6,7 +6,11 @@ channels (plus their pre-/post-MLP states) reduced to 64 tokens each.  Inputs
 are seeded synthetic tensors resident in HBM before the timed region.
 
 Prints one JSON line with images/s, the roofline of the dominant kernel (the
-fused scoring pass, HBM-bound) and the fp64 CPU oracle timed on the host.
+fused scoring pass, HBM-bound) and the fp64 CPU oracle timed on the host.  The
+default run also times the other benchmark workloads the same way (the
+single-image fp32 case as microseconds per call over 64 rotated copies of its
+buffers, so that no call finds its inputs in the 256 MB last-level cache) and
+reports them under "workloads".
 """
 from __future__ import annotations
 
@@ -55,6 +59,8 @@ def parse():
                          "inside the module (gather fused into the GEMM); timed against "
                          "tr_reduce + the library GEMM")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-workloads", action="store_true",
+                    help="time the headline workload only (no 'workloads' object)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="target wall time of the oracle sample")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -74,16 +80,28 @@ def score_source_sha() -> str:
 
 
 def measured_traffic():
-    """HBM bytes per score launch from the committed PMC summary, if it is current."""
+    """(HBM bytes per score launch or None, its source) from the committed PMC
+    summary: the figure is used only while the scoring kernel's sources still
+    hash to the ones the counters were taken on."""
+    src = {"profile": os.path.relpath(TRAFFIC_PROFILE, ROOT), "sources_sha256": score_source_sha(),
+           "what": "FETCH_SIZE + WRITE_SIZE per score_kernel dispatch (two rocprofv3 --pmc runs), "
+                   "scaled by the same counters on 512 MiB device copies"}
     try:
         text = open(TRAFFIC_PROFILE).read()
     except OSError:
-        return None
+        src["status"] = "missing"
+        return None, src
     sha = re.search(r"source_sha256:\s*([0-9a-f]{64})", text)
     byt = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
-    if not sha or not byt or sha.group(1) != score_source_sha():
-        return None
-    return float(byt.group(1))
+    if not sha or not byt:
+        src["status"] = "unreadable"
+        return None, src
+    src["profiled_sha256"] = sha.group(1)
+    if sha.group(1) != src["sources_sha256"]:
+        src["status"] = "stale: the scoring kernel changed since the counters were taken"
+        return None, src
+    src["status"] = "current"
+    return float(byt.group(1)), src
 
 
 def describe(w) -> str:
@@ -186,6 +204,111 @@ def time_events(torch, f, steps, stream):
     ev1.record(stream)
     torch.cuda.synchronize()
     return ev0.elapsed_time(ev1) / steps * 1e-3
+
+
+def needs_scores(tr, w):
+    """Which scores the plan needs (the library decides the same way): H2
+    unless lambda = 0, s unless lambda = 1."""
+    plan = tr.plan(w.N, w.K, w.lam)
+    need_x = any(0 < k1 < n for n, k1 in zip(w.N, plan[1]))
+    need_s = any(0 < k2 < n - k1 for n, k1, k2 in zip(w.N, plan[1], plan[2]))
+    return need_x, need_s
+
+
+def time_workload(torch, tr, w, steps, warmup, copies=1, stride_real=False, shannon=False):
+    """Whole steps of one workload (score -> select -> gather), timed like the
+    headline: `warmup` untimed steps, then `steps` steps between two
+    synchronizations.  With copies > 1 the steps rotate over that many copies
+    of the input and output buffers, so that no step finds its inputs in the
+    last-level cache; the per-call latency is then also taken with HIP events
+    around single calls."""
+    dev = w.X.device
+    need_x, need_s = needs_scores(tr, w)
+    r = tr.Reducer(w.D, w.Dc, w.dtype, lam=w.lam, max_images=w.B, max_tokens=sum(w.N),
+                   max_N=max(w.N), stride_real=stride_real, shannon=shannon)
+    sk = sum(w.K)
+    sets = []
+    for c in range(copies):
+        X = w.X if c == 0 else w.X.clone()
+        P = (w.Xpre if c == 0 else w.Xpre.clone()) if need_s else None
+        Q = (w.Xpost if c == 0 else w.Xpost.clone()) if need_s else None
+        sets.append((X, P, Q, torch.empty(sk, w.D, dtype=w.dtype, device=dev),
+                     torch.empty(sk, dtype=torch.int32, device=dev), torch.empty(sk, dtype=torch.uint8, device=dev)))
+    state = [0]
+
+    def step():
+        X, P, Q, out, idx, src = sets[state[0] % copies]
+        state[0] += 1
+        r.reduce(X, P, Q, w.N, w.K, out=out, out_idx=idx, out_src=src)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    res = {"ms_per_step": elapsed / steps * 1e3, "images_per_s": w.B * steps / elapsed,
+           "tokens_per_s": sum(w.N) * steps / elapsed,
+           "path_bytes": w.algorithmic_bytes(score_x=need_x, score_states=need_s), "r": r,
+           "need_x": need_x, "need_s": need_s, "step": step}
+    if copies > 1:
+        # latency of one call: events around each call, buffers rotating
+        stream = torch.cuda.current_stream(dev)
+        n = max(4 * copies, steps)
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+        torch.cuda.synchronize()
+        for e0, e1 in evs:
+            e0.record(stream)
+            step()
+            e1.record(stream)
+        torch.cuda.synchronize()
+        us = sorted(1e3 * e0.elapsed_time(e1) for e0, e1 in evs)
+        res["us_per_call"] = {"median": round(us[len(us) // 2], 2), "p10": round(us[len(us) // 10], 2),
+                              "p90": round(us[(9 * len(us)) // 10], 2), "calls": n, "buffer_copies": copies,
+                              "how": "HIP events around each call on the library's stream; inputs and outputs "
+                                     "rotate over %d copies (%.0f MB, above the 256 MB last-level cache)"
+                                     % (copies, copies * sum(t.numel() * t.element_size()
+                                                             for t in sets[0][:3] if t is not None) / 1e6)}
+    return res
+
+
+# Other benchmark workloads of the default run: (key, synth recipe, keyword
+# arguments, buffer copies, description of the configuration).
+OTHER_WORKLOADS = [
+    ("llava_k128", "llava", dict(B=64, N=576, D=4096, K=128), 1, "64 x 576 x 4096 bf16 -> 128 kept"),
+    ("llava_k192", "llava", dict(B=64, N=576, D=4096, K=192), 1, "64 x 576 x 4096 bf16 -> 192 kept"),
+    ("llava_fp32", "llava_fp32", {}, 64, "1 x 576 x 1024 fp32 -> 64 kept (latency)"),
+    ("llava_next", "llava_next", {}, 1, "16 x 2880 (5 tiles x 576) x 4096 bf16 -> 320 kept"),
+    ("qwen_ragged", "qwen_ragged", {}, 1, "32 ragged images, N in [256, 16384], 3584 bf16 -> 11 % kept"),
+    ("video", "video", {}, 1, "4 clips x 32 frames x 576 x 4096 bf16 -> 1152 kept"),
+]
+
+
+def other_workloads(torch, synth, tr, dev, steps, warmup, headline_w):
+    """The other benchmark configurations, timed like the headline."""
+    out = {}
+    for key, recipe, kw, copies, what in OTHER_WORKLOADS:
+        if recipe == "llava" and headline_w is not None:   # same tokens, another K
+            w = synth.Workload(headline_w.name, headline_w.X, headline_w.Xpre, headline_w.Xpost,
+                               list(headline_w.N), [kw["K"]] * headline_w.B, headline_w.lam)
+        else:
+            w = synth.make(recipe, device=dev, **kw)
+        t = time_workload(torch, tr, w, steps, warmup, copies=copies)
+        ms = t["ms_per_step"]
+        e = {"config": what, "images": w.B, "tokens": sum(w.N), "kept": sum(w.K),
+             "dtype": "bf16" if w.dtype == torch.bfloat16 else "f32",
+             "images_per_s": round(t["images_per_s"], 1), "tokens_per_s": round(t["tokens_per_s"], 1),
+             "ms_per_step": round(ms, 5), "path_bytes": t["path_bytes"],
+             "path_frac_of_8TBs": round(t["path_bytes"] / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+        if "us_per_call" in t:
+            e["us_per_call"] = t["us_per_call"]
+        out[key] = e
+        t["r"].close()
+        del t, w
+        torch.cuda.empty_cache()
+    return out
 
 
 def bench_fused(args, torch, synth, tr, dev):
@@ -308,34 +431,16 @@ def main():
     headline = (args.workload == "llava" and args.images == 64 and args.K == 64
                 and w.lam == synth.LAMBDA and not args.stride_real and not args.shannon)
     torch.cuda.synchronize()
-    r = tr.Reducer(w.D, w.Dc, w.dtype, lam=w.lam, max_images=w.B, max_tokens=sum(w.N),
-                   max_N=max(w.N), stride_real=args.stride_real, shannon=args.shannon)
-    # Which scores the plan needs (the library decides the same way): H2 unless
-    # lambda = 0, s unless lambda = 1.  A score that is not needed is not read.
-    plan = tr.plan(w.N, w.K, w.lam)
-    need_x = any(0 < k1 < n for n, k1 in zip(w.N, plan[1]))
-    need_s = any(0 < k2 < n - k1 for n, k1, k2 in zip(w.N, plan[1], plan[2]))
+    # Timed region: K whole steps (score -> select -> gather), nothing else.
+    # The single-image fp32 workload rotates over 64 copies of its 7 MB of
+    # buffers (its step is latency-bound and would otherwise run from cache).
+    copies = 64 if args.workload == "llava_fp32" else 1
+    t = time_workload(torch, tr, w, args.steps, args.warmup, copies=copies, stride_real=args.stride_real,
+                      shannon=args.shannon)
+    r, need_x, need_s, step = t["r"], t["need_x"], t["need_s"], t["step"]
     states = (w.Xpre, w.Xpost) if need_s else (None, None)
     xs = w.X if need_x else None
-    sk = sum(w.K)
-    out = torch.empty(sk, w.D, dtype=w.dtype, device=dev)
-    idx = torch.empty(sk, dtype=torch.int32, device=dev)
-    src = torch.empty(sk, dtype=torch.uint8, device=dev)
-
-    def step():
-        r.reduce(w.X, *states, w.N, w.K, out=out, out_idx=idx, out_src=src)
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-
-    # Timed region: K whole steps (score -> select -> gather), nothing else.
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
+    elapsed = t["ms_per_step"] * 1e-3 * args.steps
 
     # Roofline of the dominant kernel: K launches of the scoring kernel (the
     # same kernel, launch configuration and inputs as inside a step) between
@@ -412,7 +517,7 @@ def main():
     score_bytes = rows * (need_x * (w.D * e + 4) + need_s * (2 * w.Dc * e + 4))
     achieved = score_bytes / (score_ms * 1e-3) / 1e9
     path_bytes = w.algorithmic_bytes(score_x=need_x, score_states=need_s)
-    traffic = measured_traffic() if headline else None
+    traffic, traffic_source = measured_traffic() if headline else (None, None)
 
     line = {
         "metric": METRIC if headline else "images/s (%s workload%s%s%s)" % (
@@ -454,12 +559,18 @@ def main():
                      "read_ceiling_GBs": round(read_bytes / read_s / 1e9, 1),
                      "frac_of_read_ceiling": round(achieved / (read_bytes / read_s / 1e9), 4)},
     }
+    if traffic_source is not None:
+        line["roofline"]["traffic_source"] = traffic_source
+    if "us_per_call" in t:
+        line["us_per_call"] = t["us_per_call"]
+    r.close()
+    if headline and not args.no_workloads:
+        line["workloads"] = other_workloads(torch, synth, tr, dev, args.steps, args.warmup, w)
     if not args.no_cpu_baseline:
         ent, sm = (1 if args.shannon else 2), (1 if args.stride_real else 0)
         line["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds, ent, sm)
         line["cpu_baseline_all_cores"] = cpu_baseline(w, args.cpu_seconds / 2, ent, sm,
                                                       threads=min(os.cpu_count() or 1, 16))
-    r.close()
     print(json.dumps(line), flush=True)
     if args.calib_copy_mib > 0:
         n = args.calib_copy_mib << 20
