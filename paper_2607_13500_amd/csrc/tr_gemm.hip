@@ -8,7 +8,9 @@
 //     partial sums of P.C, P.P and C.C against a second [M, N] matrix P.  With
 //     C = x'' the output of the encoder MLP's second layer (W2 applied to the
 //     hidden activations) and P = x' its input, these are Eq. (6)'s three sums,
-//     so the Stage II score needs no further pass over X_pre or X_post.
+//     so the Stage II score needs no further pass over X_pre or X_post.  The
+//     sums use C as stored (rounded to bf16), so the score is Eq. (6) on the
+//     x'' the caller receives, as an unfused scoring pass would compute it.
 //
 // Two tilings for gfx950 (64-wide wavefronts, 32x32x16 bf16 MFMA), both with
 // the same per-element MFMA sequence (k ascending in steps of 16), so they give
@@ -185,8 +187,9 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmArgs a)
 #pragma unroll
             for (int j = 0; j < 2; ++j) {
                 const int n = n0 + wn * 64 + j * 32 + (lane & 31);
-                const float c = acc[i][j][v];
-                if (ok) C[(int64_t)m * a.ldc + n] = to_bf16(c);
+                const uint16_t cb = to_bf16(acc[i][j][v]);
+                const float c = bf16_lo(cb);   // the value stored
+                if (ok) C[(int64_t)m * a.ldc + n] = cb;
                 if constexpr (COS) {
                     const float p = ok ? bf16_lo(reinterpret_cast<const uint16_t*>(a.P)[(int64_t)m * a.ldp + n]) : 0.f;
                     dot = fmaf(p, c, dot);
@@ -447,7 +450,7 @@ __global__ __launch_bounds__(kWThreads, 1) void gemm_wide_kernel(GemmArgs a)
                     const int col = wn * 64 + j * 32 + l31;
                     const float pv = bf16_lo(*(const __attribute__((address_space(3))) uint16_t*)(
                         arr + (rr & 63) * 512 + col * 2));
-                    const float c = acc[i][j][v];
+                    const float c = bf16_lo(to_bf16(acc[i][j][v]));   // the value stored
                     dot = fmaf(pv, c, dot);
                     pp = fmaf(pv, pv, pp);
                     cc = fmaf(c, c, cc);
