@@ -58,6 +58,9 @@ def parse():
                     help="the step after the path: project the kept tokens by a [NOUT, D] weight "
                          "inside the module (gather fused into the GEMM); timed against "
                          "tr_reduce + the library GEMM")
+    ap.add_argument("--gemm", default="", metavar="M,N,K",
+                    help="the matrix-core GEMM core alone: C[M,N] = A[M,K] . B[N,K]^T in bf16, timed "
+                         "against the library GEMM (torch.matmul) on the same operands")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-workloads", action="store_true",
                     help="time the headline workload only (no 'workloads' object)")
@@ -311,6 +314,32 @@ def other_workloads(torch, synth, tr, dev, steps, warmup, headline_w):
     return out
 
 
+def bench_gemm(args, torch, tr, dev):
+    """The hand-written GEMM core on its own, against the library GEMM."""
+    M, N, K = (int(v) for v in args.gemm.split(","))
+    g = torch.Generator(device=dev).manual_seed(11)
+    A = torch.randn(M, K, device=dev, generator=g).to(torch.bfloat16)
+    B = (torch.randn(N, K, device=dev, generator=g) / K ** 0.5).to(torch.bfloat16)
+    C = torch.empty(M, N, device=dev, dtype=torch.bfloat16)
+    r = tr.Reducer(K, K, torch.bfloat16, max_images=1, max_tokens=1, max_N=1)
+    stream = torch.cuda.current_stream(dev)
+    t_ours = time_events(torch, lambda: r.gemm(A, B, out=C), args.steps, stream)
+    t_lib = time_events(torch, lambda: torch.matmul(A, B.t(), out=C), args.steps, stream)
+    flops = 2.0 * M * N * K
+    line = {"metric": "TFLOP/s of the bf16 GEMM core, %d x %d x %d" % (M, N, K),
+            "value": round(flops / t_ours / 1e12, 1), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": round(t_ours * 1e3, 5), "higher_is_better": True,
+            "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+            "config": {"workload": "bf16 GEMM C = A . B^T", "M": M, "N": N, "K": K},
+            "roofline": {"kernel": "gemm (tr_gemm_bf16)", "bound": "mfma", "achieved": round(flops / t_ours / 1e12, 1),
+                         "peak": 2500.0, "unit": "TFLOP/s", "frac": round(flops / t_ours / 1e12 / 2500.0, 4),
+                         "traffic": None, "avg_launch_ms": round(t_ours * 1e3, 5)},
+            "library_gemm": {"ms": round(t_lib * 1e3, 5), "tflops": round(flops / t_lib / 1e12, 1),
+                             "ratio_ours_to_library": round(t_lib / t_ours, 4)}}
+    r.close()
+    print(json.dumps(line), flush=True)
+
+
 def bench_fused(args, torch, synth, tr, dev):
     """The two fusions around the path, each against its unfused form."""
     w = synth.llava(device=dev, B=args.images, N=576, D=4096, K=args.K)
@@ -419,6 +448,9 @@ def main():
 
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
+    if args.gemm:
+        bench_gemm(args, torch, tr, dev)
+        return
     if args.mlp_fused or args.project:
         bench_fused(args, torch, synth, tr, dev)
         return
