@@ -256,6 +256,22 @@ def time_workload(torch, tr, w, steps, warmup, copies=1, stride_real=False, shan
            "tokens_per_s": sum(w.N) * steps / elapsed,
            "path_bytes": w.algorithmic_bytes(score_x=need_x, score_states=need_s), "r": r,
            "need_x": need_x, "need_s": need_s, "step": step}
+    if copies == 1:
+        # the gather's yardstick: a plain device copy (torch) of as many
+        # contiguous rows as the step keeps, between the same two buffers
+        dst, src = sets[0][3], w.X[:sk]
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        reps = 20
+        t1 = time.perf_counter()
+        for _ in range(reps):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        cs = (time.perf_counter() - t1) / reps
+        nb = 2 * dst.numel() * dst.element_size()
+        res["plain_copy"] = {"bytes": nb, "us": round(cs * 1e6, 2), "GBs": round(nb / cs / 1e9, 1),
+                             "what": "torch copy_ of the kept rows' byte count (contiguous rows), read + write"}
     if copies > 1:
         # latency of one call: events around each call, buffers rotating
         stream = torch.cuda.current_stream(dev)
@@ -307,6 +323,8 @@ def other_workloads(torch, synth, tr, dev, steps, warmup, headline_w):
              "path_frac_of_8TBs": round(t["path_bytes"] / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
         if "us_per_call" in t:
             e["us_per_call"] = t["us_per_call"]
+        if "plain_copy" in t:
+            e["plain_copy"] = t["plain_copy"]
         out[key] = e
         t["r"].close()
         del t, w
@@ -595,6 +613,8 @@ def main():
         line["roofline"]["traffic_source"] = traffic_source
     if "us_per_call" in t:
         line["us_per_call"] = t["us_per_call"]
+    if "plain_copy" in t:
+        line["plain_copy"] = t["plain_copy"]
     r.close()
     if headline and not args.no_workloads:
         line["workloads"] = other_workloads(torch, synth, tr, dev, args.steps, args.warmup, w)
