@@ -1099,8 +1099,9 @@ __global__ __launch_bounds__(kThreads) void emit_kernel(SelectArgs a)
 // ---- images of at most kSmallSelectN tokens: one token per thread ------------
 //
 // Both stages are ranked in the same passes.  Every token gets its exact rank
-// in (Stage I key, index) order and in (Stage II key, index) order among all N
-// tokens; X^imp is the ranks below K1, and a token of X^rem ranks in X^rem as
+// in (Stage II key, index) order among all N tokens, and its place relative
+// to K1 in (Stage I key, index) order (counted exactly only inside the bucket
+// that holds the K1 boundary); X^imp is the places below K1, and a token of X^rem ranks in X^rem as
 // its Stage II rank minus the X^imp tokens ranked below it (read from a
 // bitmap of X^imp in Stage II rank order), which decides the stride picks.
 // Ranks come from value buckets and exact counting inside a bucket: bucket =
@@ -1322,14 +1323,17 @@ __global__ __launch_bounds__(kSmallSelectN) void select_small_kernel(SelectArgs 
         bi1 = Si[gi + 1];
         bs0 = Ss[gs];
         bs1 = Ss[gs + 1];
-        if (bi1 - bi0 > 1u) Li[bi0 + li] = me_i;
+        // Stage I needs exact ranks only in the bucket that holds the K1
+        // boundary: a lower bucket's members are all in X^imp, a higher
+        // one's all out, whatever their order inside it.
+        if (bi1 - bi0 > 1u && bi0 < (uint32_t)K1 && bi1 > (uint32_t)K1) Li[bi0 + li] = me_i;
         if (bs1 - bs0 > 1u) Ls[bs0 + ls] = me_s;
     }
     __syncthreads();   // B5
     uint32_t ri = bi0, rs = bs0;
     if (valid) {
         if (bi.mode == 2) ri = (uint32_t)tid;
-        else if (bi1 - bi0 > 1u) ri = rank_in(Li, bi0, bi1 - bi0, me_i);
+        else if (bi1 - bi0 > 1u && bi0 < (uint32_t)K1 && bi1 > (uint32_t)K1) ri = rank_in(Li, bi0, bi1 - bi0, me_i);
         if (bs.mode == 2) rs = (uint32_t)tid;
         else if (bs1 - bs0 > 1u) rs = rank_in(Ls, bs0, bs1 - bs0, me_s);
         rs = rs < (uint32_t)N ? rs : (uint32_t)N - 1u;   // a rank below N in every case (memory safety)
