@@ -455,6 +455,44 @@ def test_capacity_and_max_n():
         run_and_check(w)
 
 
+def test_batching_and_order_do_not_change_any_image():
+    """Every image's kept indices, sources, kept rows and scores are the same
+    bit for bit whether it is reduced alone, in a ragged batch or in a
+    permuted batch.  The paths differ between these: alone, an image of at
+    most 1024 tokens takes the one-token-per-thread selection with the copy
+    fused into it, in the batch the general selection; an image with a large
+    remainder is shared by more or fewer workgroups depending on how many
+    such images its launch holds."""
+    import paper_2607_13500_amd as tr
+    w = synth.qwen_ragged(device=DEV, seed=11, B=7, n_lo=64, n_hi=9000, D=256)
+    say("ragged batch N", w.N, "K", w.K)
+    offs = np.concatenate([[0], np.cumsum(w.N)]).tolist()
+
+    def run(order):
+        Ns = [w.N[b] for b in order]
+        Ks = [w.K[b] for b in order]
+        cut = lambda t: torch.cat([t[offs[b]:offs[b + 1]] for b in order]).contiguous()
+        r = tr.Reducer(w.D, w.Dc, w.dtype, lam=w.lam, max_images=len(order), max_tokens=sum(Ns), max_N=max(Ns))
+        res = r.reduce(cut(w.X), cut(w.Xpre), cut(w.Xpost), Ns, Ks, want_scores=True)
+        torch.cuda.synchronize()
+        per, ko, to = {}, 0, 0
+        for b, n, k in zip(order, Ns, Ks):
+            per[b] = (res.idx[ko:ko + k].cpu(), res.src[ko:ko + k].cpu(),
+                      res.out[ko:ko + k].view(torch.int16).cpu(), res.h2[to:to + n].cpu(), res.s[to:to + n].cpu())
+            ko += k
+            to += n
+        r.close()
+        return per
+
+    base = run(list(range(w.B)))
+    others = [("permuted", run([3, 6, 0, 5, 1, 4, 2]))]
+    others += [("alone", run([b])) for b in range(w.B)]
+    for what, got in others:
+        for b, v in got.items():
+            for name, x, y in zip(("idx", "src", "out", "h2", "s"), base[b], v):
+                assert torch.equal(x, y), (what, b, w.N[b], name)
+
+
 def test_many_large_images_one_workgroup_each():
     """More images with large remainders than half the compute units: the
     launch gives each image one workgroup, which ranks all of its buckets a
