@@ -455,7 +455,8 @@ def test_capacity_and_max_n():
         run_and_check(w)
 
 
-def test_batching_and_order_do_not_change_any_image():
+@pytest.mark.parametrize("variant", ["algorithm-1", "stride-real", "shannon"])
+def test_batching_and_order_do_not_change_any_image(variant):
     """Every image's kept indices, sources, kept rows and scores are the same
     bit for bit whether it is reduced alone, in a ragged batch or in a
     permuted batch.  The paths differ between these: alone, an image of at
@@ -465,14 +466,16 @@ def test_batching_and_order_do_not_change_any_image():
     such images its launch holds."""
     import paper_2607_13500_amd as tr
     w = synth.qwen_ragged(device=DEV, seed=11, B=7, n_lo=64, n_hi=9000, D=256)
-    say("ragged batch N", w.N, "K", w.K)
+    say("ragged batch N", w.N, "K", w.K, variant)
     offs = np.concatenate([[0], np.cumsum(w.N)]).tolist()
+    flags = dict(stride_real=variant == "stride-real", shannon=variant == "shannon")
 
     def run(order):
         Ns = [w.N[b] for b in order]
         Ks = [w.K[b] for b in order]
         cut = lambda t: torch.cat([t[offs[b]:offs[b + 1]] for b in order]).contiguous()
-        r = tr.Reducer(w.D, w.Dc, w.dtype, lam=w.lam, max_images=len(order), max_tokens=sum(Ns), max_N=max(Ns))
+        r = tr.Reducer(w.D, w.Dc, w.dtype, lam=w.lam, max_images=len(order), max_tokens=sum(Ns), max_N=max(Ns),
+                       **flags)
         res = r.reduce(cut(w.X), cut(w.Xpre), cut(w.Xpost), Ns, Ks, want_scores=True)
         torch.cuda.synchronize()
         per, ko, to = {}, 0, 0
