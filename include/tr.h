@@ -205,8 +205,12 @@ tr_status tr_gemm_bf16(tr_ctx* ctx, const void* A, int64_t lda,
 /* The encoder MLP's second layer with Eq. (6) fused into its epilogue (Sec.
  * "Stage II": x' and x'' are the input and output of the last MLP, Eq. 5):
  *   X_post[M, Dc] = Hact[M, Hd] . W2[Dc, Hd]^T   (bf16 out, as tr_gemm_bf16)
- *   key_s[M]      = cos(X_pre[m], X_post[m]) from the fp32 accumulators
+ *   key_s[M]      = cos(X_pre[m], X_post[m]) of the X_post values as stored
+ *                   (rounded to bf16), summed in fp32 while the tile is in
+ *                   registers
  * so the Stage II key is ready without another pass over X_pre or X_post.
+ * It is Eq. (6) of the X_post the caller receives, as tr_reduce's scoring
+ * computes it up to the order of the fp32 sums.
  *   Hact   device bf16 [M, Hd] hidden activations sigma(W1 x'), row stride ldh
  *   W2     device bf16 [Dc, Hd], row stride ldw
  *   X_pre  device bf16 [M, Dc] (x'), X_post device bf16 [M, Dc] (written)
