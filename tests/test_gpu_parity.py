@@ -343,15 +343,24 @@ def _select_keys(rng, shape, total):
     return ki, ks
 
 
-def _select_against_oracle(cases, rng, stride_real):
+def _at_offset(a, off):
+    """a on the device, starting `off` floats past a 256-byte aligned base."""
+    buf = torch.zeros(a.size + off + 4, dtype=torch.float32, device=DEV)
+    v = buf[off:off + a.size]
+    v.copy_(torch.from_numpy(a))
+    return v
+
+
+def _select_against_oracle(cases, rng, stride_real, offsets=(0, 0)):
     import paper_2607_13500_amd as tr
     for ci, (N, K, lam, shape) in enumerate(cases):
-        say("select keys case", ci, "B", len(N), "lam", lam, "shape", shape, "stride_real", stride_real)
+        say("select keys case", ci, "B", len(N), "lam", lam, "shape", shape, "stride_real", stride_real,
+            "key offsets", offsets)
         total = sum(N)
         ki, ks = _select_keys(rng, shape, total)
         r = tr.Reducer(8, 8, torch.bfloat16, lam=lam, max_images=len(N), max_tokens=total,
                        max_N=max(N), stride_real=stride_real)
-        idx, src = r.select(torch.from_numpy(ki).to(DEV), torch.from_numpy(ks).to(DEV), N, K)
+        idx, src = r.select(_at_offset(ki, offsets[0]), _at_offset(ks, offsets[1]), N, K)
         idx, src = idx.cpu().numpy(), src.cpu().numpy()
         r0 = o0 = 0
         for n, k in zip(N, K):
@@ -369,6 +378,15 @@ def test_select_bit_exact_on_given_keys():
     """Integer work: with the same fp32 keys, the GPU selection equals the oracle's exactly."""
     rng = np.random.default_rng(11)
     _select_against_oracle(_select_cases(rng), rng, stride_real=False)
+
+
+@pytest.mark.parametrize("offsets", [(1, 3), (2, 0), (3, 1)])
+def test_select_bit_exact_on_misaligned_keys(offsets):
+    """Key arrays whose bases are 4, 8 or 12 bytes past a 16-byte boundary
+    (each kind its own offset): tr_select takes any 4-byte aligned key array
+    and still equals the oracle's selection."""
+    rng = np.random.default_rng(13 + offsets[0])
+    _select_against_oracle(_select_cases(rng, trials=12), rng, stride_real=False, offsets=offsets)
 
 
 def test_select_bit_exact_stride_real():
