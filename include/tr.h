@@ -90,7 +90,18 @@ typedef enum {
      * the one its score improves on (Sec. "Stage I").  The Stage I key is
      * then KL = log D - H1 (ascending = descending H1) and out_h2 receives
      * H1.  Costs a logarithm per element of X. */
-    TR_FLAG_SHANNON = 2
+    TR_FLAG_SHANNON = 2,
+    /* Count the scored rows that hold a NaN or an infinite element (the
+     * paper defines the scores for finite tokens only; such rows still get
+     * memory-safe, unspecified keys).  The context keeps a device count,
+     * zero at tr_create, to which every scoring launch (tr_reduce and its
+     * fused forms, tr_score) adds one per row that holds a non-finite
+     * element in a tensor the launch reads: X when H2 is computed, X_pre or
+     * X_post when s is computed (a row counts once).  tr_nonfinite_rows
+     * reads it.  Finite rows cost nothing extra: a non-finite element always
+     * sends its row to the scoring kernel's second read, where the check is
+     * made.  Not available to tr_reduce_noalloc (TR_EUNSUPPORTED). */
+    TR_FLAG_CHECK_FINITE = 4
 } tr_flag;
 
 /* Problem statement and capacities, fixed for the life of a context. */
@@ -262,6 +273,14 @@ tr_status tr_check_reduce(const tr_params* p, const void* X, const void* X_pre, 
 tr_status tr_plan(const tr_params* p, int32_t B, const int32_t* N,
                   const int32_t* K, int32_t* Kout, int32_t* K1out,
                   int32_t* K2out, int32_t* tout);
+
+/* With TR_FLAG_CHECK_FINITE: enqueue on `stream` a copy of the context's
+ * count of non-finite rows (see the flag) into *count (device uint32, 4-byte
+ * aligned), and, if reset != 0, set the count back to 0 in the same launch.
+ * Ordered with the caller's other work on `stream`, so the count covers the
+ * calls enqueued before it on that stream.  TR_EUNSUPPORTED for a context
+ * created without the flag. */
+tr_status tr_nonfinite_rows(tr_ctx* ctx, uint32_t* count, int32_t reset, void* stream);
 
 /* Largest N a context on the current device can select in on-chip memory. */
 int32_t tr_capacity_N(void);

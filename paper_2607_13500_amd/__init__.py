@@ -137,13 +137,15 @@ class Reducer:
     stride_real selects the real-interval variant of the diversity stride
     (positions floor(j R / K2) of the sorted remainder instead of j t);
     shannon ranks Stage I by Shannon entropy instead of Renyi-2 (the key is
-    then log D - H1 and the returned h2 holds H1).
+    then log D - H1 and the returned h2 holds H1); check_finite makes the
+    context count the scored rows that hold a NaN or infinite element
+    (nonfinite_rows reads the count).
     """
 
     def __init__(self, D: int, Dc: Optional[int] = None, dtype: torch.dtype = torch.bfloat16,
                  lam: float = LAMBDA_PAPER, keep_ratio: Optional[float] = None,
                  max_images: int = 256, max_tokens: int = 1 << 20, max_N: Optional[int] = None,
-                 device=None, stride_real: bool = False, shannon: bool = False):
+                 device=None, stride_real: bool = False, shannon: bool = False, check_finite: bool = False):
         if not torch.cuda.is_available():
             raise RuntimeError("paper_2607_13500_amd needs a ROCm GPU (gfx950)")
         self.device = torch.device("cuda", torch.cuda.current_device() if device is None
@@ -155,7 +157,7 @@ class Reducer:
             max_N = min(capacity_N_on(self.device), int(max_tokens))
         self.max_images, self.max_tokens, self.max_N = int(max_images), int(max_tokens), int(max_N)
         self.stride_real, self.shannon = bool(stride_real), bool(shannon)
-        flags = _flags(stride_real, shannon)
+        flags = _flags(stride_real, shannon) | (_lib.TR_FLAG_CHECK_FINITE if check_finite else 0)
         p = _params(D, Dc, dtype, lam, keep_ratio, max_images, max_tokens, max_N, flags)
         ctx = ctypes.c_void_p()
         with torch.cuda.device(self.device):
@@ -374,6 +376,14 @@ class Reducer:
         return idx, src
 
     # -- measurement --------------------------------------------------------
+    def nonfinite_rows(self, reset: bool = False, stream=None) -> int:
+        """The context's count of scored rows holding a NaN or infinite element
+        (a context created with check_finite=True); waits for the stream."""
+        out = torch.zeros(1, dtype=torch.int32, device=self.device)
+        _check(self.lib.tr_nonfinite_rows(self._ctx, _ptr(out), 1 if reset else 0, self._stream(stream)),
+               "tr_nonfinite_rows")
+        return int(out.item())
+
     def timing(self, enable: bool = True):
         _check(self.lib.tr_timing_enable(self._ctx, 1 if enable else 0), "tr_timing_enable")
 

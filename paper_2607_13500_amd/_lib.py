@@ -35,6 +35,7 @@ TR_OK, TR_EINVAL, TR_ENOMEM, TR_EUNSUPPORTED, TR_EDEVICE = range(5)
 TR_FP32, TR_BF16 = 0, 1
 TR_FLAG_STRIDE_REAL = 1
 TR_FLAG_SHANNON = 2
+TR_FLAG_CHECK_FINITE = 4
 TR_NOALLOC_MAX_TOKENS = 524288
 TR_NOALLOC_MAX_IMAGES = 256
 
@@ -59,6 +60,8 @@ def load(build_if_missing: bool = True) -> ctypes.CDLL:
     lib.tr_reduce.restype = i32
     lib.tr_score.argtypes = [vp, vp, vp, vp, i64, vp, vp, vp, vp]
     lib.tr_score.restype = i32
+    lib.tr_nonfinite_rows.argtypes = [vp, vp, i32, vp]
+    lib.tr_nonfinite_rows.restype = i32
     lib.tr_select.argtypes = [vp, vp, vp, i32, vp, vp, vp, vp, vp]
     lib.tr_select.restype = i32
     lib.tr_gemm_bf16.argtypes = [vp, vp, i64, vp, i64, vp, i64, vp, i64, i32, i32, i32, vp]

@@ -79,6 +79,15 @@ struct CtxAlloc {
     }
 };
 
+// Copies the context's count to a caller's word (and resets it if asked).
+__global__ void take_kernel(uint32_t* src, uint32_t* dst, int32_t reset)
+{
+    if (threadIdx.x == 0) {
+        *dst = *src;
+        if (reset) *src = 0u;
+    }
+}
+
 struct DeviceGuard {
     int prev = -1;
     bool ok = true;
@@ -110,6 +119,7 @@ struct tr_ctx {
     uint32_t* gsel = nullptr;     // pick bitmaps of images shared by several workgroups
     uint32_t* gimp = nullptr;     // their X^imp bitmaps
     float* cos_part = nullptr;    // per-tile cosine partials of tr_mlp_out_cos (bf16, Dc % 128 == 0)
+    uint32_t* nonfinite = nullptr;   // count of scored rows with a NaN or infinite element (TR_FLAG_CHECK_FINITE)
     bool timing = false;
     std::vector<hipEvent_t> events;   // 4 per timed call
     int timed = 0;
@@ -254,6 +264,17 @@ tr_status tr_create(const tr_params* p, tr_ctx** out)
         tr_destroy(c);
         return hip_fail(e, "hipFuncSetAttribute");
     }
+    if (p->flags & TR_FLAG_CHECK_FINITE) {
+        if ((e = al(&c->nonfinite, sizeof(uint32_t))) != hipSuccess) {
+            tr_destroy(c);
+            return fail(TR_ENOMEM, "hipMalloc of the non-finite row count failed");
+        }
+        if ((e = hipMemset(c->nonfinite, 0, sizeof(uint32_t))) != hipSuccess ||
+            (e = hipDeviceSynchronize()) != hipSuccess) {
+            tr_destroy(c);
+            return hip_fail(e, "non-finite row count initialisation");
+        }
+    }
     if (p->dtype == TR_BF16 && c->Dc % 128 == 0) {
         const size_t words = n * (size_t)tr::gemm_part_cols(c->Dc) * 3;
         if ((e = al(&c->cos_part, words * sizeof(float))) != hipSuccess) {
@@ -275,6 +296,7 @@ void tr_destroy(tr_ctx* c)
     if (c->gsel) (void)hipFree(c->gsel);
     if (c->gimp) (void)hipFree(c->gimp);
     if (c->cos_part) (void)hipFree(c->cos_part);
+    if (c->nonfinite) (void)hipFree(c->nonfinite);
     for (hipEvent_t ev : c->events) (void)hipEventDestroy(ev);
     delete c;
 }
@@ -426,6 +448,7 @@ tr_status reduce_impl(tr_ctx* c, ReduceCall r)
         sa.out_h2 = r.out_h2;
         sa.out_s = r.out_s;
         sa.logD = (float)log((double)c->p.D);
+        sa.nonfinite = c->nonfinite;
         if ((e = tr::launch_score(sa, c->p.dtype == TR_BF16, vec_score, mode, s)) != hipSuccess)
             return hip_fail(e, "score kernel launch");
     }
@@ -616,6 +639,21 @@ tr_status tr_read_bandwidth(const void* const* p, const int64_t* bytes, int32_t 
     return TR_OK;
 }
 
+tr_status tr_nonfinite_rows(tr_ctx* c, uint32_t* count, int32_t reset, void* stream)
+{
+    clear_error();
+    if (!c) return fail(TR_EINVAL, "ctx is NULL");
+    if (!c->nonfinite) return fail(TR_EUNSUPPORTED, "the context was created without TR_FLAG_CHECK_FINITE");
+    if (!count || ((uintptr_t)count & 3u)) return fail(TR_EINVAL, "count must be a 4-byte aligned device word");
+    DeviceGuard g(c->device);
+    if (!g.ok) return fail(TR_EDEVICE, "hipSetDevice(%d) failed", c->device);
+    hipLaunchKernelGGL(take_kernel, dim3(1), dim3(64), 0, static_cast<hipStream_t>(stream), c->nonfinite, count,
+                       reset);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "count copy launch");
+    return TR_OK;
+}
+
 tr_status tr_score(tr_ctx* c, const void* X, const void* X_pre, const void* X_post, int64_t rows,
                    float* key_imp, float* key_s, float* out_h2, void* stream)
 {
@@ -652,6 +690,7 @@ tr_status tr_score(tr_ctx* c, const void* X, const void* X_pre, const void* X_po
     sa.out_h2 = out_h2;
     sa.out_s = nullptr;
     sa.logD = (float)log((double)c->p.D);
+    sa.nonfinite = c->nonfinite;
     int mode = (want_x ? tr::kScoreImp : 0) | (want_c ? tr::kScoreSim : 0);
     if (want_x && (c->p.flags & TR_FLAG_SHANNON)) mode |= tr::kScoreShannon;
     hipError_t e = tr::launch_score(sa, c->p.dtype == TR_BF16, vec, mode, static_cast<hipStream_t>(stream));
@@ -757,6 +796,8 @@ extern "C" tr_status tr_reduce_noalloc(const tr_params* p, const void* X, const 
     clear_error();
     tr_status st = check_params(p, false);
     if (st != TR_OK) return st;
+    if (p->flags & TR_FLAG_CHECK_FINITE)
+        return fail(TR_EUNSUPPORTED, "TR_FLAG_CHECK_FINITE needs a context (tr_create) to hold its count");
     if (B > kStaticImages)
         return fail(TR_EINVAL, "B = %d exceeds the %d images of the no-allocation scratch", B, kStaticImages);
     if (B > 0 && N) {

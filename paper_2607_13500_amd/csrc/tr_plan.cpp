@@ -35,7 +35,7 @@ tr_status check_params(const tr_params* p, bool need_caps)
     if (p->Dc < 0) return fail(TR_EINVAL, "Dc must be >= 0 (got %d)", p->Dc);
     if (p->dtype != TR_FP32 && p->dtype != TR_BF16)
         return fail(TR_EINVAL, "dtype must be TR_FP32 or TR_BF16 (got %d)", p->dtype);
-    if (p->flags & ~(int32_t)(TR_FLAG_STRIDE_REAL | TR_FLAG_SHANNON))
+    if (p->flags & ~(int32_t)(TR_FLAG_STRIDE_REAL | TR_FLAG_SHANNON | TR_FLAG_CHECK_FINITE))
         return fail(TR_EINVAL, "unknown flags 0x%x", (unsigned)p->flags);
     if (!(p->lambda >= 0.0 && p->lambda <= 1.0))
         return fail(TR_EINVAL, "lambda must be in [0, 1] (got %g)", p->lambda);

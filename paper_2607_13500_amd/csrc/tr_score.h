@@ -22,6 +22,8 @@ struct ScoreArgs {
     float* out_h2;       // [rows] H2 (Shannon: H1), or nullptr
     float* out_s;        // [rows] or nullptr
     float logD;          // log(D) in fp32
+    uint32_t* nonfinite; // one is added per row holding a NaN or infinite element among the
+                         // tensors the launch reads, or nullptr: no count
 };
 
 // Which scores a launch computes (a bit set, never 0).  A score left out

@@ -33,6 +33,10 @@
 // other row is scored again from a second read, each of x' and x'' scaled by
 // the power of two of its own maximum |x|, in fp32 fused multiply-adds.
 //
+// Non-finite elements: a NaN or an infinity makes the first pass's sums NaN
+// or infinite, so such a row always takes the second read, which is where it
+// is detected; with a count requested, lane 0 adds one per such row.
+//
 // Lane partial sums are combined by a fixed DPP scan tree (the total is read
 // from lane 63 into every lane) and lane 0 writes the results.
 //
@@ -305,6 +309,7 @@ struct XRow {
     Shift h;
     float sd, sd2;
     bool zero;
+    bool nonfinite;   // some element is a NaN or infinite
 };
 
 template <bool BF16, bool H1>
@@ -313,13 +318,16 @@ __device__ __noinline__ XRow x_reread(const char* row, int D, int lane)
     XRow r;
     r.sd = r.sd2 = 0.f;
     float mx = 0.f, mn = __builtin_inff();
+    bool bad = false;
     for (int j = lane; j < D; j += kWave) {
         const float a = fabsf(elem<BF16>(row, j));
         mx = fmaxf(mx, a);
         mn = fminf(mn, a);
+        bad = bad || !(a <= 3.40282347e38f);   // NaN or infinite
     }
     const float rmax = wave_max_nonneg(mx);
     const float rmin = wave_min_nonneg(mn);
+    r.nonfinite = __any(bad) != 0;
     r.zero = !(rmax > 0.f && rmax <= 3.40282347e38f);
     if (r.zero) {
         r.h = make_shift(0.f, 1.f);
@@ -343,19 +351,28 @@ __device__ __noinline__ XRow x_reread(const char* row, int D, int lane)
     return r;
 }
 
+struct CRow {
+    float s;
+    bool nonfinite;   // some element of x' or x'' is a NaN or infinite
+};
+
 // Eq. (6) from a second read of the two rows, each scaled by the power of two
 // of its own maximum |x| (s is invariant to both), in fp32 fused
 // multiply-adds.  A zero vector gives s = 0.
 template <bool BF16>
-__device__ __noinline__ float cos_reread(const char* pr, const char* qr, int Dc, int lane)
+__device__ __noinline__ CRow cos_reread(const char* pr, const char* qr, int Dc, int lane)
 {
     float mp = 0.f, mq = 0.f;
+    bool bad = false;
     for (int j = lane; j < Dc; j += kWave) {
-        mp = fmaxf(mp, fabsf(elem<BF16>(pr, j)));
-        mq = fmaxf(mq, fabsf(elem<BF16>(qr, j)));
+        const float u = fabsf(elem<BF16>(pr, j)), v = fabsf(elem<BF16>(qr, j));
+        mp = fmaxf(mp, u);
+        mq = fmaxf(mq, v);
+        bad = bad || !(u <= 3.40282347e38f) || !(v <= 3.40282347e38f);   // NaN or infinite
     }
+    CRow r{0.f, __any(bad) != 0};
     const float xp = wave_max_nonneg(mp), xq = wave_max_nonneg(mq);
-    if (!(xp > 0.f) || !(xq > 0.f)) return 0.f;
+    if (!(xp > 0.f) || !(xq > 0.f)) return r;
     const float sp = binade_scale(xp), sq = binade_scale(xq);
     float dot = 0.f, n1 = 0.f, n2 = 0.f;
     for (int j = lane; j < Dc; j += kWave) {
@@ -367,7 +384,8 @@ __device__ __noinline__ float cos_reread(const char* pr, const char* qr, int Dc,
     dot = wave_sum(dot);
     n1 = wave_sum(n1);
     n2 = wave_sum(n2);
-    return dot / (sqrtf(n1) * sqrtf(n2));
+    r.s = dot / (sqrtf(n1) * sqrtf(n2));
+    return r;
 }
 
 template <bool BF16, bool VEC, int UNR, int MODE>
@@ -471,6 +489,9 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a)
 
     float sd = 0.f, sd2 = 0.f, s = 0.f;
     bool zero_row = false;
+    // A NaN or infinite element always sends its row to a second read (its
+    // sums leave the range the first pass accepts), which reports it.
+    bool bad_row = false;
     if constexpr (kX) {
         sd = wave_sum(xa.sd);
         sd2 = wave_sum(xa.sd2);
@@ -478,6 +499,7 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a)
         // score the row again from its maximum (a wave-uniform decision).
         if (!(fast_x && sd2 <= 0x1p100f)) {
             const XRow r = x_reread<BF16, kH1>(xr, a.D, lane);
+            bad_row = r.nonfinite;
             sh = r.h;
             sd = r.sd;
             sd2 = r.sd2;
@@ -486,10 +508,13 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a)
     }
     if constexpr (kC) {
         const float dot = wave_sum(ca.dot), n1 = wave_sum(ca.n1), n2 = wave_sum(ca.n2);
-        if (n1 >= 0x1p-60f && n2 >= 0x1p-60f && n1 <= 3.40282347e38f && n2 <= 3.40282347e38f)
+        if (n1 >= 0x1p-60f && n2 >= 0x1p-60f && n1 <= 3.40282347e38f && n2 <= 3.40282347e38f) {
             s = dot / (sqrtf(n1) * sqrtf(n2));
-        else
-            s = cos_reread<BF16>(pr, qr, a.Dc, lane);
+        } else {
+            const CRow r = cos_reread<BF16>(pr, qr, a.Dc, lane);
+            s = r.s;
+            bad_row = bad_row || r.nonfinite;
+        }
     }
 
     if (lane == 0) {
@@ -531,6 +556,7 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a)
         if (a.key_s) a.key_s[row] = s;
         if (kX && a.out_h2) a.out_h2[row] = h2;
         if (kC && a.out_s) a.out_s[row] = s;
+        if (a.nonfinite && bad_row) atomicAdd(a.nonfinite, 1u);
     }
 }
 

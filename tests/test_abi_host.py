@@ -138,7 +138,7 @@ def test_create_rejects_bad_params_before_touching_a_device():
     good = dict(D=64, Dc=0, dtype=1, max_images=4, max_tokens=1024, max_N=512, flags=0,
                 lam=1 / 3, keep_ratio=0.0)
     bad = [dict(D=0), dict(Dc=-1), dict(dtype=7), dict(max_images=0), dict(max_tokens=0),
-           dict(max_tokens=1 << 31), dict(max_N=0), dict(flags=4), dict(flags=-1), dict(lam=2.0),
+           dict(max_tokens=1 << 31), dict(max_N=0), dict(flags=8), dict(flags=-1), dict(lam=2.0),
            dict(keep_ratio=-0.5)]
     for b in bad:
         p = _lib.Params(**{**good, **b})
@@ -154,7 +154,24 @@ def test_null_context_calls_are_rejected():
     assert lib.tr_reduce(None, None, None, None, 1, N, None, None, None, None, None, None, None) == _lib.TR_EINVAL
     assert lib.tr_select(None, None, None, 1, N, None, None, None, None) == _lib.TR_EINVAL
     assert lib.tr_score(None, None, None, None, 1, None, None, None, None) == _lib.TR_EINVAL
+    assert lib.tr_nonfinite_rows(None, None, 0, None) == _lib.TR_EINVAL
     lib.tr_destroy(None)
+
+
+def test_every_variant_flag_is_accepted_and_others_are_not():
+    """TR_FLAG_STRIDE_REAL, TR_FLAG_SHANNON and TR_FLAG_CHECK_FINITE (and
+    their combinations) pass the host checks; any other bit is TR_EINVAL."""
+    lib = _lib.load()
+    N = (ctypes.c_int32 * 1)(100)
+    K = (ctypes.c_int32 * 1)(10)
+    g = 1 << 20
+    known = _lib.TR_FLAG_STRIDE_REAL | _lib.TR_FLAG_SHANNON | _lib.TR_FLAG_CHECK_FINITE
+    for flags in range(16):
+        p = _lib.Params(D=64, Dc=0, dtype=_lib.TR_BF16, max_images=0, max_tokens=0, max_N=0, flags=flags,
+                        lam=1.0 / 3.0, keep_ratio=0.0)
+        want = _lib.TR_OK if flags & ~known == 0 else _lib.TR_EINVAL
+        assert lib.tr_check_reduce(ctypes.byref(p), g, g, g, 1, N, K, g, g, None, None, None) == want, flags
+        assert lib.tr_plan(ctypes.byref(p), 1, N, K, None, None, None, None) == want, flags
 
 
 def test_gemm_and_fused_entry_points_validate_before_touching_a_device():

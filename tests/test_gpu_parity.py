@@ -570,6 +570,88 @@ def test_non_finite_inputs_give_well_formed_output(N, dtype):
     r.close()
 
 
+@pytest.mark.parametrize("shannon", [False, True])
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+def test_check_finite_counts_the_nonfinite_rows(dtype, shannon):
+    """TR_FLAG_CHECK_FINITE: the context counts every scored row that holds a
+    NaN or an infinite element, once per row, among the tensors the call
+    reads (X when H2 is computed, X_pre / X_post when s is); huge finite
+    values are not counted.  The count accumulates over calls until read with
+    reset.  On finite rows nothing is counted and every result equals that of
+    a context without the flag, bit for bit."""
+    import ctypes
+    import paper_2607_13500_amd as tr
+    from paper_2607_13500_amd import _lib
+    say("check finite", dtype, "shannon", shannon)
+    g = torch.Generator().manual_seed(77)
+    N, D, Dc, K = 600, 256, 200, 60
+    X = torch.randn(N, D, generator=g)
+    P = torch.randn(N, Dc, generator=g)
+    Q = torch.randn(N, Dc, generator=g)
+    X[3, 5] = float("nan")
+    X[7] = float("inf")
+    X[11, :10] = float("-inf")
+    X[13] = float("nan")
+    X[40, 100] = float("nan")
+    X[29, 0] = 3.0e38                  # finite
+    P[17, 0] = float("nan")
+    P[40, 3] = float("inf")            # the same row as an X entry: counted once
+    Q[19] = float("inf")
+    P[23] = 3.0e38                     # finite
+    x_rows, c_rows = {3, 7, 11, 13, 40}, {17, 19, 40}
+    cast = lambda t: t.to(dtype).to(DEV).contiguous()
+    Xd, Pd, Qd = cast(X), cast(P), cast(Q)
+
+    def ctx(lam):
+        return tr.Reducer(D, Dc, dtype, lam=lam, max_images=1, max_tokens=N, max_N=N, shannon=shannon,
+                          check_finite=True)
+
+    r = ctx(synth.LAMBDA)
+    r.reduce(Xd, Pd, Qd, [N], [K])
+    assert r.nonfinite_rows() == len(x_rows | c_rows)
+    r.reduce(Xd, Pd, Qd, [N], [K], want_scores=True)
+    assert r.nonfinite_rows(reset=True) == 2 * len(x_rows | c_rows)
+    assert r.nonfinite_rows() == 0
+    r.score(Xd, Pd, Qd)
+    assert r.nonfinite_rows(reset=True) == len(x_rows | c_rows)
+    r.close()
+    r = ctx(1.0)                                   # s decides nothing: the states are not read
+    r.reduce(Xd, Pd, Qd, [N], [K])
+    assert r.nonfinite_rows() == len(x_rows)
+    r.close()
+    r = ctx(0.0)                                   # H2 decides nothing: X is only gathered
+    r.reduce(Xd, Pd, Qd, [N], [K])
+    assert r.nonfinite_rows() == len(c_rows)
+    r.close()
+    # finite rows: no count, and the same bits as without the flag
+    w = synth.llava(device=DEV, B=3, N=577, D=520, K=100, dtype=dtype)
+    a = tr.Reducer(w.D, w.Dc, w.dtype, lam=w.lam, max_images=3, max_tokens=sum(w.N), max_N=577, shannon=shannon,
+                   check_finite=True)
+    b = tr.Reducer(w.D, w.Dc, w.dtype, lam=w.lam, max_images=3, max_tokens=sum(w.N), max_N=577, shannon=shannon)
+    ra = a.reduce(w.X, w.Xpre, w.Xpost, w.N, w.K, want_scores=True)
+    rb = b.reduce(w.X, w.Xpre, w.Xpost, w.N, w.K, want_scores=True)
+    assert a.nonfinite_rows() == 0
+    assert torch.equal(ra.idx, rb.idx) and torch.equal(ra.src, rb.src)
+    assert torch.equal(ra.h2.view(torch.int32), rb.h2.view(torch.int32))
+    assert torch.equal(ra.s.view(torch.int32), rb.s.view(torch.int32))
+    assert torch.equal(ra.out.view(torch.uint8), rb.out.view(torch.uint8))
+    with pytest.raises(tr.TRError) as e:           # only a context holds the count
+        b.nonfinite_rows()
+    assert e.value.status == _lib.TR_EUNSUPPORTED
+    a.close()
+    b.close()
+    p = _lib.Params(D=w.D, Dc=w.Dc, dtype=_lib.TR_BF16 if dtype == torch.bfloat16 else _lib.TR_FP32, max_images=0,
+                    max_tokens=0, max_N=0, flags=_lib.TR_FLAG_CHECK_FINITE, lam=w.lam, keep_ratio=0.0)
+    out = torch.empty(sum(w.K), w.D, dtype=dtype, device=DEV)
+    idx = torch.empty(sum(w.K), dtype=torch.int32, device=DEV)
+    Nh = (ctypes.c_int32 * 3)(*w.N)
+    Kh = (ctypes.c_int32 * 3)(*w.K)
+    st = _lib.load().tr_reduce_noalloc(ctypes.byref(p), w.X.data_ptr(), w.Xpre.data_ptr(), w.Xpost.data_ptr(), 3,
+                                       Nh, Kh, out.data_ptr(), idx.data_ptr(), None, None, None, None)
+    assert st == _lib.TR_EUNSUPPORTED
+    torch.cuda.synchronize()
+
+
 # ------------------------------------------------------ stream ordering
 
 ORDER_CASES = [
