@@ -6,6 +6,8 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <dlfcn.h>
+
 #include <algorithm>
 #include <atomic>
 #include <mutex>
@@ -20,6 +22,7 @@ using tr::check_params;
 using tr::clear_error;
 using tr::elem_bytes;
 using tr::fail;
+using tr::log_line;
 using tr::ImageDesc;
 using tr::make_plan;
 using tr::Plan;
@@ -55,6 +58,53 @@ int capacity_for(int lds_limit)
 }
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+// Optional roctx ranges: with the environment variable TR_ROCTX = 1 the
+// marker library is opened once (dlopen, no link-time dependency) and every
+// entry point that enqueues work brackets its enqueue in a range named after
+// itself, so a marker trace ties each call to the kernels it launched.
+struct Roctx {
+    int (*push)(const char*) = nullptr;
+    int (*pop)() = nullptr;
+};
+
+const Roctx& roctx()
+{
+    static const Roctx r = [] {
+        Roctx x;
+        const char* v = getenv("TR_ROCTX");
+        if (!v || strcmp(v, "1") != 0) return x;
+        void* h = dlopen("librocprofiler-sdk-roctx.so.1", RTLD_NOW | RTLD_LOCAL);
+        if (!h) h = dlopen("libroctx64.so.4", RTLD_NOW | RTLD_LOCAL);
+        if (!h) {
+            log_line("TR_ROCTX=1 but no roctx library could be opened");
+            return x;
+        }
+        x.push = reinterpret_cast<int (*)(const char*)>(dlsym(h, "roctxRangePushA"));
+        x.pop = reinterpret_cast<int (*)()>(dlsym(h, "roctxRangePop"));
+        if (!x.push || !x.pop) {
+            x.push = nullptr;
+            x.pop = nullptr;
+            log_line("TR_ROCTX=1 but the roctx library lacks its range functions");
+        } else {
+            log_line("roctx ranges on");
+        }
+        return x;
+    }();
+    return r;
+}
+
+struct Range {
+    bool on;
+    explicit Range(const char* name) : on(roctx().push != nullptr)
+    {
+        if (on) roctx().push(name);
+    }
+    ~Range()
+    {
+        if (on) roctx().pop();
+    }
+};
 
 // The device allocations of one tr_create call.  Test hook: with the
 // environment variable TR_FAIL_ALLOC = k (k >= 1), the k-th allocation fails
@@ -282,6 +332,10 @@ tr_status tr_create(const tr_params* p, tr_ctx** out)
             return fail(TR_ENOMEM, "hipMalloc of %zu cosine partials failed", words);
         }
     }
+    log_line("context on device %d: D %d, Dc %d, %s, lambda %.6g, flags 0x%x, up to %d images / %lld tokens / "
+             "N %d (device selection capacity %d)",
+             dev, p->D, c->Dc, p->dtype == TR_BF16 ? "bf16" : "fp32", p->lambda, (unsigned)p->flags, p->max_images,
+             (long long)p->max_tokens, p->max_N, cap);
     *out = c;
     return TR_OK;
 }
@@ -488,6 +542,7 @@ tr_status tr_reduce(tr_ctx* c, const void* X, const void* X_pre, const void* X_p
                     uint8_t* out_src, float* out_h2, float* out_s, void* stream)
 {
     clear_error();
+    Range range("tr_reduce");
     ReduceCall r;
     r.X = X;
     r.X_pre = X_pre;
@@ -509,6 +564,7 @@ tr_status tr_reduce_given_s(tr_ctx* c, const void* X, const float* key_s, int32_
                             void* stream)
 {
     clear_error();
+    Range range("tr_reduce_given_s");
     if (!key_s) return fail(TR_EINVAL, "key_s must be non-NULL");
     ReduceCall r;
     r.X = X;
@@ -529,6 +585,7 @@ tr_status tr_reduce_project(tr_ctx* c, const void* X, const void* X_pre, const v
                             void* out, int32_t* out_idx, uint8_t* out_src, void* stream)
 {
     clear_error();
+    Range range("tr_reduce_project");
     if (!W) return fail(TR_EINVAL, "W must be non-NULL");
     ReduceCall r;
     r.X = X;
@@ -552,6 +609,7 @@ tr_status tr_gemm_bf16(tr_ctx* c, const void* A, int64_t lda, const int32_t* a_r
                        void* stream)
 {
     clear_error();
+    Range range("tr_gemm_bf16");
     if (!c) return fail(TR_EINVAL, "ctx is NULL");
     if (M < 0) return fail(TR_EINVAL, "M must be >= 0");
     if (!tr::gemm_shape_ok(M, N, K))
@@ -585,6 +643,7 @@ tr_status tr_mlp_out_cos(tr_ctx* c, const void* Hact, int64_t ldh, const void* W
                          const void* X_pre, void* X_post, int32_t M, int32_t Hd, float* key_s, void* stream)
 {
     clear_error();
+    Range range("tr_mlp_out_cos");
     if (!c) return fail(TR_EINVAL, "ctx is NULL");
     if (c->p.dtype != TR_BF16) return fail(TR_EUNSUPPORTED, "tr_mlp_out_cos needs a bf16 context");
     if (!c->cos_part) return fail(TR_EUNSUPPORTED, "tr_mlp_out_cos needs Dc %% 128 == 0 (Dc = %d)", c->Dc);
@@ -623,6 +682,7 @@ tr_status tr_read_bandwidth(const void* const* p, const int64_t* bytes, int32_t 
                             int32_t sink_words, void* stream)
 {
     clear_error();
+    Range range("tr_read_bandwidth");
     if (n < 1 || n > tr::kReadBuffers || !p || !bytes)
         return fail(TR_EINVAL, "n must be in [1, %d] with host arrays p and bytes", tr::kReadBuffers);
     int64_t total = 0;
@@ -658,6 +718,7 @@ tr_status tr_score(tr_ctx* c, const void* X, const void* X_pre, const void* X_po
                    float* key_imp, float* key_s, float* out_h2, void* stream)
 {
     clear_error();
+    Range range("tr_score");
     if (!c) return fail(TR_EINVAL, "ctx is NULL");
     if (rows < 0) return fail(TR_EINVAL, "rows must be >= 0");
     if (rows == 0) return TR_OK;
@@ -702,6 +763,7 @@ tr_status tr_select(tr_ctx* c, const float* key_imp, const float* key_s, int32_t
                     const int32_t* K, int32_t* out_idx, uint8_t* out_src, void* stream)
 {
     clear_error();
+    Range range("tr_select");
     if (!c) return fail(TR_EINVAL, "ctx is NULL");
     Plan pl;
     tr_status st = check_ctx_plan(c, B, N, K, pl);

@@ -6,6 +6,8 @@
 #include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
 
 namespace tr {
 
@@ -15,12 +17,30 @@ thread_local char g_err[512];
 
 void clear_error() { g_err[0] = '\0'; }
 
+bool log_enabled()
+{
+    const char* v = getenv("TR_LOG");
+    return v && strcmp(v, "1") == 0;
+}
+
+void log_line(const char* fmt, ...)
+{
+    if (!log_enabled()) return;
+    char line[640];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(line, sizeof line, fmt, ap);
+    va_end(ap);
+    fprintf(stderr, "tr: %s\n", line);
+}
+
 tr_status fail(tr_status st, const char* fmt, ...)
 {
     va_list ap;
     va_start(ap, fmt);
     vsnprintf(g_err, sizeof g_err, fmt, ap);
     va_end(ap);
+    if (log_enabled()) fprintf(stderr, "tr: %s: %s\n", tr_strerror(st), g_err);
     return st;
 }
 

@@ -57,10 +57,13 @@ struct Plan {
 };
 
 // Latest failure of the calling thread, kept in a fixed buffer (reporting
-// allocates nothing).
+// allocates nothing).  With the environment variable TR_LOG = 1 every failure
+// is also written to stderr as one line, and log_line writes other lines
+// (context creation); otherwise the library prints nothing.
 void clear_error();
 tr_status fail(tr_status st, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
 const char* last_error();
+void log_line(const char* fmt, ...) __attribute__((format(printf, 1, 2)));
 
 int elem_bytes(int32_t dtype);
 

@@ -292,3 +292,50 @@ def test_check_reduce_states_the_alignment_rule():
         assert chk(P=None, Q=None) == _lib.TR_OK
         assert chk(P=g + 1, Q=g + 1) == _lib.TR_OK
         assert chk(P=None, Q=None, s=g) == _lib.TR_EINVAL       # asking for s needs the states
+
+
+def _run_with_env(env_extra, code):
+    env = dict(os.environ)
+    env.update(env_extra)
+    return subprocess.run(["python3", "-c", code], capture_output=True, text=True, env=env, cwd=ROOT, timeout=300)
+
+
+_BAD_PLAN = """
+import ctypes
+from paper_2607_13500_amd import _lib
+lib = _lib.load()
+p = _lib.Params(D=0, Dc=0, dtype=1, max_images=0, max_tokens=0, max_N=0, flags=0, lam=0.5, keep_ratio=0.0)
+N = (ctypes.c_int32 * 1)(4)
+print(lib.tr_plan(ctypes.byref(p), 1, N, None, None, None, None, None))
+print(lib.tr_read_bandwidth(None, None, 0, None, 0, None))
+"""
+
+
+def test_log_is_opt_in():
+    """The library prints nothing unless TR_LOG=1; then each failure is one
+    stderr line naming the status and the reason."""
+    quiet = _run_with_env({"TR_LOG": "0"}, _BAD_PLAN)
+    assert quiet.returncode == 0, quiet.stderr
+    assert quiet.stdout.split() == [str(_lib.TR_EINVAL)] * 2
+    assert "tr:" not in quiet.stderr
+    loud = _run_with_env({"TR_LOG": "1"}, _BAD_PLAN)
+    assert loud.returncode == 0, loud.stderr
+    lines = [l for l in loud.stderr.splitlines() if l.startswith("tr: ")]
+    assert len(lines) == 2, loud.stderr
+    assert lines[0].startswith("tr: invalid argument: ") and "D" in lines[0]
+    assert "n must be in [1, 8]" in lines[1]
+
+
+def test_roctx_ranges_are_opt_in_and_harmless():
+    """TR_ROCTX=1 opens the roctx library at the first entry point that
+    enqueues work and brackets each such call in a range (here calls that
+    fail their argument checks, so no device is needed); the process runs
+    and ends normally with the ranges balanced.  Without it no range is
+    made."""
+    on = _run_with_env({"TR_ROCTX": "1", "TR_LOG": "1"}, _BAD_PLAN)
+    assert on.returncode == 0, on.stderr
+    assert on.stdout.split() == [str(_lib.TR_EINVAL)] * 2
+    assert "tr: roctx ranges on" in on.stderr, on.stderr
+    off = _run_with_env({"TR_ROCTX": "0", "TR_LOG": "1"}, _BAD_PLAN)
+    assert off.returncode == 0, off.stderr
+    assert "roctx" not in off.stderr, off.stderr
