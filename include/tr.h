@@ -50,10 +50,11 @@
  * Environment (all optional, for diagnosis): TR_LOG = 1 writes every failure
  * (and a one-line description of each context at tr_create) to stderr; the
  * library prints nothing otherwise.  TR_ROCTX = 1 opens the roctx marker
- * library at the first call that enqueues work and brackets each such call
- * (tr_reduce, its fused forms, tr_score, tr_select, tr_gemm_bf16,
- * tr_read_bandwidth) in a range named after the entry point, so that a
- * profiler's marker trace ties every call to its kernels.  TR_FAIL_ALLOC and
+ * library at the first call that enqueues work and brackets each call of
+ * tr_reduce, tr_reduce_given_s, tr_reduce_project, tr_score, tr_select,
+ * tr_gemm_bf16, tr_mlp_out_cos and tr_read_bandwidth in a range named after
+ * the entry point, so that a profiler's marker trace ties every call to its
+ * kernels.  TR_FAIL_ALLOC and
  * TR_GEMM_TILE_ROWS are test hooks described at tr_create and tr_gemm_bf16.
  *
  * Alignment: every tensor base must be aligned to its element size (2 bytes
