@@ -5,8 +5,10 @@
  * checks what C alone can check (per image: K strictly ascending in-range
  * indices, K1 = floor(lambda K) of them from Stage I, the kept rows equal to
  * X's rows byte for byte), and writes the inputs and outputs as raw arrays to
- * the directory given as its argument, for the oracle comparison of the test
- * that builds it.  Exit status 0 when every call and check succeeded. */
+ * the directory given as its first argument, for the oracle comparison of the
+ * test that builds it.  An optional second argument picks the element type
+ * and variant: "fp32" (default), "bf16", "bf16-shannon" or "fp32-stride-real".
+ * Exit status 0 when every call and check succeeded. */
 #include <math.h>
 #include <stdint.h>
 #include <stdio.h>
@@ -54,6 +56,23 @@ static float normal(void)   /* Box-Muller */
     return sqrtf(-2.0f * logf(u1)) * cosf(6.28318531f * u2);
 }
 
+/* fp32 -> bf16, round to nearest even (finite inputs) */
+static uint16_t to_bf16(float f)
+{
+    uint32_t u;
+    memcpy(&u, &f, 4);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+static float from_bf16(uint16_t h)
+{
+    const uint32_t u = (uint32_t)h << 16;
+    float f;
+    memcpy(&f, &u, 4);
+    return f;
+}
+
 static int write_file(const char* dir, const char* name, const void* p, size_t bytes)
 {
     char path[4096];
@@ -70,10 +89,19 @@ static int write_file(const char* dir, const char* name, const void* p, size_t b
 
 int main(int argc, char** argv)
 {
-    if (argc != 2) {
-        fprintf(stderr, "usage: %s <output directory>\n", argv[0]);
+    if (argc != 2 && argc != 3) {
+        fprintf(stderr, "usage: %s <output directory> [fp32|bf16|bf16-shannon|fp32-stride-real]\n", argv[0]);
         return 2;
     }
+    const char* mode = argc == 3 ? argv[2] : "fp32";
+    const int bf16 = strncmp(mode, "bf16", 4) == 0;
+    const int32_t flags = strcmp(mode, "bf16-shannon") == 0 ? TR_FLAG_SHANNON
+                          : strcmp(mode, "fp32-stride-real") == 0 ? TR_FLAG_STRIDE_REAL : 0;
+    if (!bf16 && strcmp(mode, "fp32") != 0 && strcmp(mode, "fp32-stride-real") != 0) {
+        fprintf(stderr, "unknown mode %s\n", mode);
+        return 2;
+    }
+    const size_t eb = bf16 ? 2 : 4;
     int64_t rows = 0, kept = 0;
     for (int b = 0; b < NIMG; ++b) {
         rows += kN[b];
@@ -101,18 +129,39 @@ int main(int argc, char** argv)
         }
     }
 
+    /* the element arrays the library reads: fp32 as generated, or bf16 (and
+     * the fp32 arrays set to the rounded values, for the checks below) */
+    void* hX = X;
+    void* hP = P;
+    void* hQ = Q;
+    uint16_t *bX = NULL, *bP = NULL, *bQ = NULL;
+    if (bf16) {
+        bX = malloc(2 * (size_t)(rows * D));
+        bP = malloc(2 * (size_t)(rows * DC));
+        bQ = malloc(2 * (size_t)(rows * DC));
+        if (!bX || !bP || !bQ) return 1;
+        for (int64_t i = 0; i < rows * D; ++i) X[i] = from_bf16(bX[i] = to_bf16(X[i]));
+        for (int64_t i = 0; i < rows * DC; ++i) {
+            P[i] = from_bf16(bP[i] = to_bf16(P[i]));
+            Q[i] = from_bf16(bQ[i] = to_bf16(Q[i]));
+        }
+        hX = bX;
+        hP = bP;
+        hQ = bQ;
+    }
+
     void *dX, *dP, *dQ, *dout, *didx, *dsrc, *dh2, *ds;
-    HIP_OK(hipMalloc(&dX, sizeof(float) * (size_t)(rows * D)));
-    HIP_OK(hipMalloc(&dP, sizeof(float) * (size_t)(rows * DC)));
-    HIP_OK(hipMalloc(&dQ, sizeof(float) * (size_t)(rows * DC)));
-    HIP_OK(hipMalloc(&dout, sizeof(float) * (size_t)(kept * D)));
+    HIP_OK(hipMalloc(&dX, eb * (size_t)(rows * D)));
+    HIP_OK(hipMalloc(&dP, eb * (size_t)(rows * DC)));
+    HIP_OK(hipMalloc(&dQ, eb * (size_t)(rows * DC)));
+    HIP_OK(hipMalloc(&dout, eb * (size_t)(kept * D)));
     HIP_OK(hipMalloc(&didx, sizeof(int32_t) * (size_t)kept));
     HIP_OK(hipMalloc(&dsrc, (size_t)kept));
     HIP_OK(hipMalloc(&dh2, sizeof(float) * (size_t)rows));
     HIP_OK(hipMalloc(&ds, sizeof(float) * (size_t)rows));
-    HIP_OK(hipMemcpy(dX, X, sizeof(float) * (size_t)(rows * D), hipMemcpyHostToDevice));
-    HIP_OK(hipMemcpy(dP, P, sizeof(float) * (size_t)(rows * DC), hipMemcpyHostToDevice));
-    HIP_OK(hipMemcpy(dQ, Q, sizeof(float) * (size_t)(rows * DC), hipMemcpyHostToDevice));
+    HIP_OK(hipMemcpy(dX, hX, eb * (size_t)(rows * D), hipMemcpyHostToDevice));
+    HIP_OK(hipMemcpy(dP, hP, eb * (size_t)(rows * DC), hipMemcpyHostToDevice));
+    HIP_OK(hipMemcpy(dQ, hQ, eb * (size_t)(rows * DC), hipMemcpyHostToDevice));
     hipStream_t stream;
     HIP_OK(hipStreamCreate(&stream));
 
@@ -120,11 +169,11 @@ int main(int argc, char** argv)
     memset(&p, 0, sizeof p);
     p.D = D;
     p.Dc = DC;
-    p.dtype = TR_FP32;
+    p.dtype = bf16 ? TR_BF16 : TR_FP32;
     p.max_images = NIMG;
     p.max_tokens = rows;
     p.max_N = 1000;
-    p.flags = 0;
+    p.flags = flags;
     p.lambda = 1.0 / 3.0;
     p.keep_ratio = 0.0;
     tr_ctx* ctx = NULL;
@@ -132,7 +181,11 @@ int main(int argc, char** argv)
     TR_OK_OR_FAIL(tr_reduce(ctx, dX, dP, dQ, NIMG, kN, kK, dout, (int32_t*)didx, (uint8_t*)dsrc, (float*)dh2,
                             (float*)ds, (void*)stream));
     HIP_OK(hipStreamSynchronize(stream));
-    HIP_OK(hipMemcpy(out, dout, sizeof(float) * (size_t)(kept * D), hipMemcpyDeviceToHost));
+    uint16_t* bout = bf16 ? malloc(2 * (size_t)(kept * D)) : NULL;
+    if (bf16 && !bout) return 1;
+    HIP_OK(hipMemcpy(bf16 ? (void*)bout : (void*)out, dout, eb * (size_t)(kept * D), hipMemcpyDeviceToHost));
+    if (bf16)
+        for (int64_t i = 0; i < kept * D; ++i) out[i] = from_bf16(bout[i]);
     HIP_OK(hipMemcpy(idx, didx, sizeof(int32_t) * (size_t)kept, hipMemcpyDeviceToHost));
     HIP_OK(hipMemcpy(src, dsrc, (size_t)kept, hipMemcpyDeviceToHost));
     HIP_OK(hipMemcpy(h2, dh2, sizeof(float) * (size_t)rows, hipMemcpyDeviceToHost));
@@ -184,6 +237,10 @@ int main(int argc, char** argv)
     free(src);
     free(h2);
     free(s);
-    printf("c client ok: %d images, %lld tokens, %lld kept\n", NIMG, (long long)rows, (long long)kept);
+    free(bX);
+    free(bP);
+    free(bQ);
+    free(bout);
+    printf("c client ok (%s): %d images, %lld tokens, %lld kept\n", mode, NIMG, (long long)rows, (long long)kept);
     return 0;
 }
