@@ -78,6 +78,53 @@ def test_noalloc_equals_reduce_on_consecutive_calls():
     _same(ref4, got4, "call 4")
 
 
+def test_noalloc_replays_from_a_hip_graph():
+    """Work under HIP graph capture is one of the callers the entry point is
+    for: a captured call (including a split selection, whose bitmaps live in
+    the shared static array) replays bit for bit like tr_reduce, with eager
+    calls of the entry point on other inputs between the replays."""
+    import paper_2607_13500_amd as tr
+    say("no-alloc under graph capture: 1 clip of 8 x 576 tokens + 3 images of 576, D 1024 bf16")
+    clip = synth.video(device=DEV, B=1, frames=8, positions=576, D=1024, K=288)
+    imgs = synth.llava(device=DEV, B=3, N=576, D=1024, K=64)
+    ref, _ = _both(clip)
+    sk, rows = sum(clip.K), sum(clip.N)
+    out = torch.empty(sk, clip.D, dtype=clip.dtype, device=DEV)
+    idx = torch.empty(sk, dtype=torch.int32, device=DEV)
+    src = torch.empty(sk, dtype=torch.uint8, device=DEV)
+    h2 = torch.empty(rows, device=DEV)
+    s = torch.empty(rows, device=DEV)
+
+    def call():
+        tr.reduce_noalloc(clip.X, clip.Xpre, clip.Xpost, clip.N, clip.K, out=out, out_idx=idx, out_src=src,
+                          out_h2=h2, out_s=s, lam=clip.lam)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):   # warm-up on the capture stream (the array is set up by now)
+        call()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=side):
+        call()
+    torch.cuda.synchronize()
+    for rep in range(3):
+        out.zero_()
+        idx.fill_(-1)
+        src.fill_(7)
+        h2.fill_(float("nan"))
+        s.fill_(float("nan"))
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        _same(ref, tr.ReduceResult(out, idx, src, h2, s), "replay %d" % rep)
+        # eager use of the same static array on other inputs between replays
+        ref2, got2 = _both(imgs)
+        _same(ref2, got2, "eager call between replays %d" % rep)
+    del graph
+
+
 def test_noalloc_rejects_calls_beyond_its_scratch():
     import paper_2607_13500_amd as tr
     from paper_2607_13500_amd import _lib
