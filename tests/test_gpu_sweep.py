@@ -73,3 +73,45 @@ def test_random_case_matches_oracle(seed, c):
     # every excused pick instead)
     assert rep.ok(), rep.failures[:5]
     r.close()
+
+
+def test_one_context_across_many_random_calls():
+    """State does not leak between calls: one context (and the static array
+    of the no-allocation entry) driven through a sequence of random calls of
+    changing shape, long images whose selection is split between workgroups
+    among them, gives each call's result bit for bit as a fresh context does."""
+    import paper_2607_13500_amd as tr
+    rng = random.Random(4242)
+    D, Dc, cap_tokens, cap_images, cap_N = 256, 192, 60000, 40, 18432
+    long_lived = tr.Reducer(D, Dc, torch.bfloat16, lam=1 / 3, max_images=cap_images, max_tokens=cap_tokens,
+                            max_N=cap_N)
+    for call in range(40):
+        B = rng.choice([1, 2, 3, 7, 33])
+        Ns = []
+        for _ in range(B):
+            n = rng.choice([1, 64, 577, 1000, 2880, 4200, 9000, 18432])
+            Ns.append(max(1, min(n, (cap_tokens - sum(Ns)) // max(1, B - len(Ns)))))
+        Ks = [max(1, min(n, rng.choice([1, n // 16 + 1, n // 3 + 1, n]))) for n in Ns]
+        g = torch.Generator(device="cpu").manual_seed(900 + call)
+        rows = sum(Ns)
+        X = (torch.randn(rows, D, generator=g) * torch.exp(torch.randn(rows, 1, generator=g))).to(torch.bfloat16)
+        P = torch.randn(rows, Dc, generator=g).to(torch.bfloat16)
+        Q = (P.float() + torch.randn(rows, Dc, generator=g)).to(torch.bfloat16)
+        X, P, Q = X.to(DEV), P.to(DEV), Q.to(DEV)
+        print("[case] long-lived context call %d: B=%d N=%s" % (call, B, Ns), flush=True)
+        got = long_lived.reduce(X, P, Q, Ns, Ks, want_scores=True)
+        fresh = tr.Reducer(D, Dc, torch.bfloat16, lam=1 / 3, max_images=B, max_tokens=rows, max_N=max(Ns))
+        want = fresh.reduce(X, P, Q, Ns, Ks, want_scores=True)
+        sk = sum(Ks)
+        na = tr.reduce_noalloc(X, P, Q, Ns, Ks, out=torch.empty(sk, D, dtype=torch.bfloat16, device=DEV),
+                               out_idx=torch.empty(sk, dtype=torch.int32, device=DEV),
+                               out_src=torch.empty(sk, dtype=torch.uint8, device=DEV),
+                               out_h2=torch.empty(rows, device=DEV), out_s=torch.empty(rows, device=DEV))
+        torch.cuda.synchronize()
+        for other, what in ((got, "long-lived context"), (na, "no-allocation entry")):
+            assert torch.equal(other.idx, want.idx) and torch.equal(other.src, want.src), (call, what)
+            assert torch.equal(other.out.view(torch.int16), want.out.view(torch.int16)), (call, what)
+            assert torch.equal(other.h2.view(torch.int32), want.h2.view(torch.int32)), (call, what)
+            assert torch.equal(other.s.view(torch.int32), want.s.view(torch.int32)), (call, what)
+        fresh.close()
+    long_lived.close()
