@@ -295,12 +295,14 @@ tr_status tr_nonfinite_rows(tr_ctx* ctx, uint32_t* count, int32_t reset, void* s
 /* Largest N a context on the current device can select in on-chip memory. */
 int32_t tr_capacity_N(void);
 
-/* Per-stage kernel timing for measurement: when enabled, tr_reduce records
- * HIP events around its score, select and gather kernels on the caller's
- * stream.  tr_timing_read waits for the recorded calls, writes the summed
- * milliseconds of each stage into ms[3] (score, select, gather) and the
- * number of calls into *calls, then clears the record.  At most 1024 calls
- * are kept between reads (later calls are not timed). */
+/* Per-stage kernel timing for measurement: when enabled, tr_reduce (and
+ * tr_reduce_given_s, tr_reduce_project) records HIP events around its score,
+ * select and gather (or projection) kernels on the caller's stream.
+ * tr_timing_read waits for the recorded calls, writes the summed milliseconds
+ * of each stage into ms[3] (score, select, gather) and the number of calls
+ * into *calls, then clears the record.  At most 1024 calls are kept between
+ * reads (later calls are not timed); a call that returns an error is not
+ * counted. */
 tr_status tr_timing_enable(tr_ctx* ctx, int32_t enable);
 tr_status tr_timing_read(tr_ctx* ctx, double* ms, int64_t* calls);
 

@@ -173,7 +173,6 @@ struct tr_ctx {
     bool timing = false;
     std::vector<hipEvent_t> events;   // 4 per timed call
     int timed = 0;
-    int64_t untimed = 0;
 };
 
 namespace {
@@ -369,7 +368,6 @@ tr_status tr_timing_enable(tr_ctx* c, int32_t enable)
     }
     c->timing = enable != 0;
     c->timed = 0;
-    c->untimed = 0;
     return TR_OK;
 }
 
@@ -395,7 +393,6 @@ tr_status tr_timing_read(tr_ctx* c, double* ms, int64_t* calls)
     ms[2] = acc[2];
     if (calls) *calls = c->timed;
     c->timed = 0;
-    c->untimed = 0;
     return TR_OK;
 }
 
@@ -481,11 +478,11 @@ tr_status reduce_impl(tr_ctx* c, ReduceCall r)
     DeviceGuard g(c->device);
     if (!g.ok) return fail(TR_EDEVICE, "hipSetDevice(%d) failed", c->device);
     hipStream_t s = static_cast<hipStream_t>(r.stream);
+    // A timed call takes the next free slot of four events; the slot counts
+    // only once every launch of the call is enqueued, so a call that fails
+    // part-way leaves no half-recorded slot for tr_timing_read.
     hipEvent_t* ev = nullptr;
-    if (c->timing) {
-        if (c->timed < kTimedCalls) ev = &c->events[(size_t)(c->timed++) * 4];
-        else ++c->untimed;
-    }
+    if (c->timing && c->timed < kTimedCalls) ev = &c->events[(size_t)c->timed * 4];
     hipError_t e;
     if (ev && (e = hipEventRecord(ev[0], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
 
@@ -530,6 +527,7 @@ tr_status reduce_impl(tr_ctx* c, ReduceCall r)
     else if (!fc.X) e = tr::launch_gather(r.X, r.out, c->rows, pl.sum_k, pl.sum_n, row_bytes, c->eb, vec_gather, s);
     if (e != hipSuccess) return hip_fail(e, r.W ? "projection kernel launch" : "gather kernel launch");
     if (ev && (e = hipEventRecord(ev[3], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    if (ev) ++c->timed;
     return TR_OK;
 }
 

@@ -673,8 +673,14 @@ def test_reduce_is_ordered_on_the_callers_stream(name, kw):
     r = reducer_for(w)
     r.timing(True)
     ref_run = r.reduce(w.X, w.Xpre, w.Xpost, w.N, w.K, want_scores=True)
+    with pytest.raises(tr.TRError):   # rejected before any launch: not timed
+        r.reduce(w.X, w.Xpre, w.Xpost, w.N, [n + 1 for n in w.N], want_scores=True)
     torch.cuda.synchronize()
-    r.timing_read()
+    ms, calls = r.timing_read()
+    # score and select each run a kernel; the gather stage is empty when the
+    # selection copies the kept rows itself
+    assert calls == 1 and ms[0] > 0 and ms[1] > 0 and ms[2] >= 0, (ms, calls)
+    assert r.timing_read()[1] == 0
     r.timing(False)
     for stream in (torch.cuda.current_stream(), torch.cuda.Stream()):
         with torch.cuda.stream(stream):
