@@ -667,6 +667,7 @@ def test_reduce_is_ordered_on_the_callers_stream(name, kw):
     host synchronisation, sees the finished outputs: on the null stream and on
     a stream of the caller's own, for back-to-back calls, and equal to the run
     with the per-stage timing events."""
+    import paper_2607_13500_amd as tr
     say("stream order", name, kw)
     w = synth.make(name, device=DEV, **kw)
     say("   rows", sum(w.N), "images", w.B)
