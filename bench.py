@@ -314,6 +314,9 @@ OTHER_WORKLOADS = [
     ("llava_k128", "llava", dict(B=64, N=576, D=4096, K=128), 1, "64 x 576 x 4096 bf16 -> 128 kept"),
     ("llava_k192", "llava", dict(B=64, N=576, D=4096, K=192), 1, "64 x 576 x 4096 bf16 -> 192 kept"),
     ("llava_fp32", "llava_fp32", {}, 64, "1 x 576 x 1024 fp32 -> 64 kept (latency)"),
+    # the one module timing the paper reports (Table II): one 576-token image at
+    # the encoder width 1024, K = 192 (64 by entropy + 128 by stride)
+    ("llava_fp32_k192", "llava_fp32", dict(K=192), 64, "1 x 576 x 1024 fp32 -> 192 kept (latency)"),
     ("llava_next", "llava_next", {}, 1, "16 x 2880 (5 tiles x 576) x 4096 bf16 -> 320 kept"),
     ("qwen_ragged", "qwen_ragged", {}, 1, "32 ragged images, N in [256, 16384], 3584 bf16 -> 11 % kept"),
     ("video", "video", {}, 1, "4 clips x 32 frames x 576 x 4096 bf16 -> 1152 kept"),

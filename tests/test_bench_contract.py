@@ -19,7 +19,8 @@ def test_recorded_bench_line_meets_the_contract():
     assert m, "no JSON line in the workloads profile"
     line = json.loads(m.group(1))
     assert bench_contract.problems(line) == []
-    assert set(line["workloads"]) == {"llava_k128", "llava_k192", "llava_fp32", "llava_next", "qwen_ragged", "video"}
+    assert set(line["workloads"]) == {"llava_k128", "llava_k192", "llava_fp32", "llava_fp32_k192", "llava_next",
+                                      "qwen_ragged", "video"}
 
 
 def test_validator_catches_broken_lines():
