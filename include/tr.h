@@ -29,8 +29,9 @@
  * Memory: every pointer named "device" is HIP device memory on the device
  * that was current at tr_create; host arrays are read during the call only.
  * The caller owns all tensors; a context owns only the scratch it allocates
- * in tr_create.  No other call allocates memory (tr_reduce_noalloc works in a
- * static device array of the library instead of a context's scratch).
+ * in tr_create (and the HIP events tr_timing_enable creates).  No other call
+ * allocates memory (tr_reduce_noalloc works in a static device array of the
+ * library instead of a context's scratch).
  *
  * Layout: rows are packed back to back.  Image b's rows start at
  * sum_{b' < b} N[b'] in X, X_pre, X_post (and the score outputs), and its
