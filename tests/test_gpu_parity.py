@@ -526,6 +526,18 @@ def test_many_large_images_one_workgroup_each():
     run_and_check(w)
 
 
+def test_ragged_batch_beyond_one_selection_launch():
+    """A ragged batch of more images than one selection launch describes (the
+    per-image descriptors travel in the launch's arguments, 32 to a launch):
+    the batch is selected in three launches, and every image matches the
+    oracle, long ones shared by several workgroups in the later launches
+    included."""
+    w = synth.qwen_ragged(device=DEV, seed=21, B=70, n_lo=16, n_hi=9000, D=128)
+    say("ragged batch of", w.B, "images, N", min(w.N), "..", max(w.N), "tokens", sum(w.N))
+    rep, _ = run_and_check(w, use_keep_ratio=True)
+    assert rep.images == 70
+
+
 # ------------------------------------------------------ non-finite inputs
 
 @pytest.mark.parametrize("N,dtype", [(600, torch.bfloat16), (5000, torch.bfloat16), (300, torch.float32)])
