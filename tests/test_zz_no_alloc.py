@@ -125,6 +125,31 @@ def test_noalloc_replays_from_a_hip_graph():
     del graph
 
 
+def test_noalloc_at_its_limits():
+    """Calls at the scratch's limits: the largest image count (a ragged batch,
+    selected in several launches, long images shared by several workgroups)
+    and the largest token count, each equal to tr_reduce and to the oracle."""
+    from paper_2607_13500_amd import _lib
+    B = _lib.TR_NOALLOC_MAX_IMAGES
+    say("no-alloc at the image limit:", B, "ragged images, D 64 bf16")
+    w = synth.qwen_ragged(device=DEV, seed=31, B=B, n_lo=16, n_hi=3000, D=64)
+    assert sum(w.N) <= _lib.TR_NOALLOC_MAX_TOKENS
+    ref, got = _both(w)
+    _same(ref, got, "image limit")
+    rep = parity.check(w, got, parity.oracle_reference(w))
+    print("   ", rep.summary(), flush=True)
+    assert rep.ok(), rep.failures[:5]
+    n = _lib.TR_NOALLOC_MAX_TOKENS // B
+    say("no-alloc at the token limit:", B, "x", n, "tokens, D 64 bf16")
+    w = synth.video(device=DEV, B=B, frames=1, positions=n, D=64, K=n // 8)
+    assert sum(w.N) == _lib.TR_NOALLOC_MAX_TOKENS
+    ref, got = _both(w)
+    _same(ref, got, "token limit")
+    rep = parity.check(w, got, parity.oracle_reference(w))
+    print("   ", rep.summary(), flush=True)
+    assert rep.ok(), rep.failures[:5]
+
+
 def test_noalloc_rejects_calls_beyond_its_scratch():
     import paper_2607_13500_amd as tr
     from paper_2607_13500_amd import _lib
