@@ -538,6 +538,29 @@ def test_ragged_batch_beyond_one_selection_launch():
     assert rep.images == 70
 
 
+def test_batch_beyond_4_gib_per_tensor():
+    """A batch whose tensors pass 4 GiB (1100 images of 576 x 4096 bf16, 5.2 GB
+    each of X, X_pre, X_post): every byte offset is 64-bit.  Images at the
+    start, the middle and the end of the batch match the oracle run on those
+    images alone (an image's result depends on its own rows only)."""
+    import paper_2607_13500_amd as tr
+    w = synth.llava(device=DEV, B=1100, N=576, D=4096, K=64)
+    assert w.X.numel() * w.X.element_size() > 4 << 30
+    say("batch of", w.B, "images,", sum(w.N), "tokens,", w.X.numel() * 2 / 1e9, "GB per tensor")
+    r = reducer_for(w)
+    res = r.reduce(w.X, w.Xpre, w.Xpost, w.N, w.K, want_scores=True)
+    torch.cuda.synchronize()
+    for b in (0, 1, 550, 1098, 1099):
+        t0, t1, k0, k1 = 576 * b, 576 * (b + 1), 64 * b, 64 * (b + 1)
+        sub = synth.Workload(w.name, w.X[t0:t1], w.Xpre[t0:t1], w.Xpost[t0:t1], [576], [64], w.lam)
+        got = tr.ReduceResult(res.out[k0:k1], res.idx[k0:k1], res.src[k0:k1], res.h2[t0:t1], res.s[t0:t1])
+        assert torch.equal(got.out.view(torch.int16), sub.X[got.idx.long()].view(torch.int16)), b
+        rep = parity.check(sub, got, parity.oracle_reference(sub))
+        print("    image", b, rep.summary(), flush=True)
+        assert rep.ok(), (b, rep.failures[:5])
+    r.close()
+
+
 # ------------------------------------------------------ non-finite inputs
 
 @pytest.mark.parametrize("N,dtype", [(600, torch.bfloat16), (5000, torch.bfloat16), (300, torch.float32)])
