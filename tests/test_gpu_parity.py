@@ -542,7 +542,8 @@ def test_batch_beyond_4_gib_per_tensor():
     """A batch whose tensors pass 4 GiB (1100 images of 576 x 4096 bf16, 5.2 GB
     each of X, X_pre, X_post): every byte offset is 64-bit.  Images at the
     start, the middle and the end of the batch match the oracle run on those
-    images alone (an image's result depends on its own rows only)."""
+    images alone (an image's result depends on its own rows only), and the
+    fused projection over this X equals the GEMM on the gathered copy."""
     import paper_2607_13500_amd as tr
     w = synth.llava(device=DEV, B=1100, N=576, D=4096, K=64)
     assert w.X.numel() * w.X.element_size() > 4 << 30
@@ -558,6 +559,16 @@ def test_batch_beyond_4_gib_per_tensor():
         rep = parity.check(sub, got, parity.oracle_reference(sub))
         print("    image", b, rep.summary(), flush=True)
         assert rep.ok(), (b, rep.failures[:5])
+    # the projection reading the kept rows straight from this X (past 31-bit
+    # offsets: the GEMM's register-prefetch tiling) equals the GEMM on the
+    # gathered copy (the LDS-destination tiling) bit for bit
+    g = torch.Generator(device=DEV).manual_seed(5)
+    W = (torch.randn(1024, 4096, device=DEV, generator=g) / 64).to(torch.bfloat16)
+    proj = r.reduce_project(w.X, w.Xpre, w.Xpost, w.N, w.K, W)
+    ref = r.gemm(res.out, W)
+    torch.cuda.synchronize()
+    assert torch.equal(proj.idx, res.idx)
+    assert torch.equal(proj.out.view(torch.int16), ref.view(torch.int16))
     r.close()
 
 
