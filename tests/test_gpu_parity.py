@@ -538,6 +538,30 @@ def test_ragged_batch_beyond_one_selection_launch():
     assert rep.images == 70
 
 
+def test_many_tiny_images():
+    """Thousands of images of 1 to 40 tokens (a ragged batch selected in 32
+    launches, then a uniform batch of 4096 one-token images in one launch):
+    every image against the oracle, K from 1 to N."""
+    import random
+    rng = random.Random(77)
+    N = [rng.randint(1, 40) for _ in range(1000)]
+    K = [rng.randint(1, n) for n in N]
+    g = torch.Generator(device="cpu").manual_seed(77)
+    rows = sum(N)
+    X = (torch.randn(rows, 48, generator=g) * torch.exp(torch.randn(rows, 1, generator=g))).to(torch.bfloat16)
+    P = torch.randn(rows, 40, generator=g).to(torch.bfloat16)
+    Q = (P.float() + torch.randn(rows, 40, generator=g)).to(torch.bfloat16)
+    w = synth.Workload("tiny", X.to(DEV), P.to(DEV), Q.to(DEV), N, K, synth.LAMBDA)
+    say("ragged batch of", w.B, "images of 1..40 tokens")
+    rep, _ = run_and_check(w)
+    assert rep.images == 1000
+    w = synth.Workload("tiny", X[:4096].to(DEV), P[:4096].to(DEV), Q[:4096].to(DEV), [1] * 4096, [1] * 4096,
+                       synth.LAMBDA)
+    say("uniform batch of 4096 one-token images")
+    rep, res = run_and_check(w)
+    assert torch.count_nonzero(res.idx) == 0
+
+
 def test_batch_beyond_4_gib_per_tensor():
     """A batch whose tensors pass 4 GiB (1100 images of 576 x 4096 bf16, 5.2 GB
     each of X, X_pre, X_post): every byte offset is 64-bit.  Images at the
