@@ -58,6 +58,8 @@ SMALL = [
     ("qwen_ragged", dict(B=5, n_lo=256, n_hi=3000, D=3584)),
     ("video", dict(B=1, frames=6, positions=576, D=4096, K=216)),
     ("llava", dict(B=2, N=300, D=4096, K=40, dtype=torch.float32)),   # 16 KiB rows: one per wavefront
+    ("llava", dict(B=2, N=200, D=8192, K=30, dtype=torch.float32)),   # 32 KiB rows
+    ("llava", dict(B=2, N=200, D=12288, K=30)),                       # 24 KiB bf16 rows, six loop passes
 ]
 
 
