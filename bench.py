@@ -482,6 +482,9 @@ def main():
     import synth
     import paper_2607_13500_amd as tr
 
+    if not torch.cuda.is_available():
+        print("bench.py needs a HIP device (an MI355X); none is visible", file=sys.stderr)
+        sys.exit(2)
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
     if args.gemm:
